@@ -1,0 +1,282 @@
+#!/usr/bin/env python3
+"""Benchmark of the BDLM attention hot path on one MI355X.
+
+Headline: fused BDLM attention forward + backward at 32K context (batch 1,
+L = 32768 clean + 32768 corrupted tokens, block size 64, 32 query / 8 KV heads,
+head_dim 128, bf16 inputs, fp32 accumulation, bf16 outputs), seeded synthetic
+N(0, 1) inputs resident in HBM before the timed region.  One step = one
+bdlm_attn_fwd + one bdlm_attn_bwd call (tile classification, fused forward,
+backward pre-pass, fused backward, dQ post-pass).
+
+value = useful TFLOP/s: valid query-key pairs of the mask (the paper's unit of
+attention work, App. B) x (4 d forward + 10 d backward) FLOP, divided by the
+measured step time.  Masked entries inside partly visible tiles and skipped
+tiles are never counted.
+
+Also reported on the same JSON line:
+* roofline of the dominant kernel (the fused backward), timed per launch with
+  HIP events the library records around each kernel on the launch stream;
+* per-kernel averages of the step;
+* one 256K CSBP rank's share (17 partial forwards, a 17-way LSE merge and the
+  backward over the 17 key ranges) with the merge kernel's HBM roofline;
+* cpu_baseline: the fp64 oracle timed on this host on a bounded sample of the
+  same workload (evenly spaced query rows of one head, forward + backward).
+
+Only one GPU is used: --gpus N with N > 1 exits with a message.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "BDLM attn fwd+bwd useful TFLOP/s & MFMA util at 32K ctx, 1 MI355X"
+PEAK_BF16_TFLOPS = 256 * 4096 * 2.4e9 / 1e12  # 256 CUs x 2048 bf16 FMA/clk/CU x 2 x 2.4 GHz = 2516.6
+PEAK_HBM_GBS = 8000.0
+KERNEL_SOURCES = ["common.hpp", "device.hpp", "bwd_bf16.hip"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_bwd_bf16_32k.json")
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2609_19242_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def recorded_traffic():
+    """HBM bytes per launch of the fused backward from rocprofv3 PMC runs, if taken on this kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def per_kernel(records):
+    out = {}
+    for name, ms in records:
+        d = out.setdefault(name, [0.0, 0])
+        d[0] += ms
+        d[1] += 1
+    return {k: {"avg_ms": v[0] / v[1], "launches": v[1]} for k, v in out.items()}
+
+
+def bench_32k(torch, bd, synth, steps, warmup):
+    w = synth.WORKLOADS["32k"]
+    dev = "cuda"
+    q, k, v, do = synth.make_joint(w, device=dev)
+    B, n, Hq, D = q.shape
+    L, M = w.L, w.block_size
+    p = bd.make_problem(B, L, M, Hq, w.kv_heads, D, torch.bfloat16)
+    r = bd.joint_ranges(L)
+    pairs = bd.visible_pairs(p, r, r)
+    fl = bd.useful_flops(pairs, Hq, B, D)
+    o = torch.empty_like(q)
+    lse = torch.empty((B, Hq, n), dtype=torch.float32, device=dev)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    ws = torch.empty(bd.attn_bwd_workspace_bytes(p, r), dtype=torch.uint8, device=dev)
+
+    def step():
+        bd.joint_fwd(q, k, v, M, out=(o, lse))
+        bd.joint_bwd(q, k, v, o, lse, do, M, out=(dq, dk, dv), workspace=ws)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    bd.timing_enable(True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record()
+    for _ in range(steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    bd.timing_enable(False)
+    kern = per_kernel(bd.timing_collect())
+    ms = e0.elapsed_time(e1) / steps
+    assert torch.isfinite(o).all() and torch.isfinite(dq).all()
+    for name, kd in kern.items():
+        if name == "fwd_bf16":
+            kd["useful_tflops"] = fl["fwd"] / (kd["avg_ms"] * 1e-3) / 1e12
+        elif name == "bwd_bf16":
+            kd["useful_tflops"] = fl["bwd"] / (kd["avg_ms"] * 1e-3) / 1e12
+    bwd_ms = kern["bwd_bf16"]["avg_ms"]
+    achieved = fl["bwd"] / (bwd_ms * 1e-3) / 1e12
+    roof = {"bound": "mfma", "kernel": "bwd_bf16", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": recorded_traffic(),
+            "flop_per_launch": fl["bwd"], "avg_launch_ms": bwd_ms}
+    res = {"ms_per_step": ms, "wall_s": wall, "pairs_per_head": pairs, "flops": fl, "kernels": kern,
+           "roofline": roof, "value": fl["total"] / (ms * 1e-3) / 1e12, "workload": w}
+    del q, k, v, do, o, lse, dq, dk, dv, ws
+    torch.cuda.empty_cache()
+    return res
+
+
+def bench_csbp(torch, bd, synth, steps, warmup):
+    w = synth.WORKLOADS["csbp256k"]
+    dev = "cuda"
+    q, kl, vl, kc, vc, do = synth.make_csbp_rank(w, device=dev)
+    Hq, D, n = w.heads, w.head_dim, w.local_tokens
+    p = bd.make_problem(1, w.L, w.block_size, Hq, w.kv_heads, D, torch.bfloat16)
+    qr = bd.Range(bd.CORRUPTED, w.local_pos0, n)
+    krs = [bd.Range(bd.CORRUPTED, w.local_pos0, n)] + \
+          [bd.Range(bd.CLEAN, s * w.shard_tokens, w.shard_tokens) for s in range(w.n_shards)]
+    step_b = w.shard_tokens * w.kv_heads * D * 2
+    ks = [kl.data_ptr()] + [kc.data_ptr() + s * step_b for s in range(w.n_shards)]
+    vs = [vl.data_ptr()] + [vc.data_ptr() + s * step_b for s in range(w.n_shards)]
+    dkl, dvl, dkc, dvc = (torch.empty_like(t) for t in (kl, vl, kc, vc))
+    dks = [dkl.data_ptr()] + [dkc.data_ptr() + s * step_b for s in range(w.n_shards)]
+    dvs = [dvl.data_ptr()] + [dvc.data_ptr() + s * step_b for s in range(w.n_shards)]
+    J = len(krs)
+    o_parts = [torch.empty_like(q) for _ in range(J)]
+    l_parts = [torch.empty((1, Hq, n), dtype=torch.float32, device=dev) for _ in range(J)]
+    om, dq = torch.empty_like(q), torch.empty_like(q)
+    lm = torch.empty((1, Hq, n), dtype=torch.float32, device=dev)
+    ws = torch.empty(bd.attn_bwd_workspace_bytes(p, [qr]), dtype=torch.uint8, device=dev)
+    pairs = bd.visible_pairs(p, [qr], krs)
+    fl = bd.useful_flops(pairs, Hq, 1, D)
+
+    def step():
+        for j in range(J):
+            bd.attn_partial_fwd(p, qr, q, o_parts[j], l_parts[j], krs[j], ks[j], vs[j])
+        bd.lse_merge(o_parts, l_parts, om, lm)
+        bd.attn_bwd(p, [qr], [q], [om], [lm], [do], [dq], krs, ks, vs, dks, dvs, ws)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    bd.timing_enable(True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    bd.timing_enable(False)
+    kern = per_kernel(bd.timing_collect())
+    ms = e0.elapsed_time(e1) / steps
+    # merge: algorithmic bytes.  Every part's LSE is read; O_j is read only where
+    # w_j != 0, which here is every row of the non-empty parts.
+    nonempty = int(sum(bool(torch.isfinite(l).any()) for l in l_parts))
+    rows_h = n * Hq
+    merge_bytes = nonempty * rows_h * D * 2 + J * rows_h * 4 + rows_h * D * 2 + rows_h * 4
+    mms = kern["lse_merge"]["avg_ms"]
+    gbs = merge_bytes / (mms * 1e-3) / 1e9
+    res = {"workload": w.describe(), "ms_per_step": ms, "useful_tflops": fl["total"] / (ms * 1e-3) / 1e12,
+           "pairs_per_head": pairs, "kernels": kern,
+           "merge_roofline": {"bound": "hbm", "kernel": "lse_merge", "achieved": gbs, "peak": PEAK_HBM_GBS,
+                              "unit": "GB/s", "frac": gbs / PEAK_HBM_GBS, "bytes_per_launch": merge_bytes,
+                              "parts": J, "parts_read": nonempty}}
+    return res
+
+
+def cpu_baseline(bd, synth, budget_s):
+    """The fp64 oracle on the host: forward + backward of evenly spaced query rows of one head of the 32K workload."""
+    import numpy as np
+    import oracle
+    w = synth.WORKLOADS["32k"]
+    L, M, D = w.L, w.block_size, w.head_dim
+    q, k, v, do = synth.make_joint(w, device="cpu")
+    h = 0
+    kv = h // (w.heads // w.kv_heads)
+    k0 = k[:, :, kv:kv + 1].double().numpy()
+    v0 = v[:, :, kv:kv + 1].double().numpy()
+    r = oracle.joint_ranges(L)
+    s_all, p_all = oracle.rows_of(r)
+    chunk_rows = 64
+    n_chunks = (2 * L) // chunk_rows
+    order = np.random.default_rng(0).permutation(n_chunks)
+    pairs = 0
+    rows_done = 0
+    t0 = time.perf_counter()
+    for c in order:
+        rows = list(range(c * chunk_rows, (c + 1) * chunk_rows))
+        single = [(int(s_all[i]), int(p_all[i]), 1) for i in rows]
+        qs, dos = q[:, rows, h:h + 1], do[:, rows, h:h + 1]
+        O, LSE = oracle.fwd(qs, k0, v0, single, r, M)
+        oracle.bwd(qs, k0, v0, O, LSE, dos, single, r, M)
+        pairs += oracle.count_visible_pairs(single, r, M)
+        rows_done += len(rows)
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    el = time.perf_counter() - t0
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:
+        cores = len(os.sched_getaffinity(0))
+    flops = 14 * D * pairs
+    return {"value": flops / el / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+            "sample": f"{rows_done} query rows (random 64-row chunks) x 1 head of the 32K workload, "
+                      f"fp64 forward+backward over all their visible keys ({pairs} pairs) in {el:.1f} s",
+            "seconds": el}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--cpu-budget-s", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-csbp", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only (the data-parallel hot path of one rank); "
+              f"--gpus {args.gpus} / WORLD_SIZE={world} is not supported", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2609_19242_amd as bd
+    import synth
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    bd.lib()  # fail loudly if the HIP library is missing
+
+    main_res = bench_32k(torch, bd, synth, args.steps, args.warmup)
+    print(f"[bench] 32k: {main_res['ms_per_step']:.3f} ms/step, {main_res['value']:.1f} useful TFLOP/s", flush=True)
+    csbp = None if args.no_csbp else bench_csbp(torch, bd, synth, max(2, args.steps // 2), 1)
+    if csbp:
+        print(f"[bench] csbp256k: {csbp['ms_per_step']:.3f} ms/step", flush=True)
+    cpu = None if args.no_cpu_baseline else cpu_baseline(bd, synth, args.cpu_budget_s)
+    w = main_res["workload"]
+    line = {
+        "metric": METRIC,
+        "value": main_res["value"],
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": main_res["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.describe(), "batch": w.batch, "L": w.L, "block_size": w.block_size,
+                   "heads": w.heads, "kv_heads": w.kv_heads, "head_dim": w.head_dim, "clean_intra": "causal",
+                   "parallelism": "single GPU"},
+        "mfma_util_useful": main_res["value"] / PEAK_BF16_TFLOPS,
+        "useful_flop_per_step": main_res["flops"]["total"],
+        "roofline": main_res["roofline"],
+        "kernels": main_res["kernels"],
+        "cpu_baseline": cpu,
+        "csbp256k": csbp,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,280 @@
+"""MI355X (gfx950) BDLM attention: Python binding of ``libbdlm_attn.so``.
+
+The C ABI (``include/bdlm_attn.h``) does all the work in HIP kernels; this
+module only marshals arguments: it builds the ``bdlm_problem`` / ``bdlm_range``
+records, passes tensor data pointers and torch's current HIP stream, turns
+status codes into exceptions, and allocates outputs with torch.
+
+``torch`` is imported before the library is loaded so that the library binds
+to the HIP runtime torch already holds (both carry the soname
+``libamdhip64.so.7``).  If the library has not been built, every call raises:
+there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import List, Optional, Sequence
+
+import torch  # noqa: F401  (load torch's HIP runtime first)
+
+__all__ = [
+    "Problem", "Range", "BdlmError", "lib", "library_path",
+    "BF16", "F32", "CLEAN", "CORRUPTED", "CLEAN_INTRA_CAUSAL", "CLEAN_INTRA_BLOCK",
+    "make_problem", "joint_ranges", "attn_fwd", "attn_partial_fwd", "lse_merge",
+    "attn_bwd_workspace_bytes", "attn_bwd", "visible_pairs",
+    "joint_fwd", "joint_bwd", "timing_enable", "timing_collect", "useful_flops",
+]
+
+BF16, F32 = 0, 1
+CLEAN, CORRUPTED = 0, 1
+CLEAN_INTRA_CAUSAL, CLEAN_INTRA_BLOCK = 0, 1
+MAX_Q_RANGES, MAX_K_RANGES, MAX_MERGE_PARTS = 4, 32, 32
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+library_path = os.path.join(_HERE, "libbdlm_attn.so")
+
+
+class Problem(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int64), ("L", ctypes.c_int64), ("block_size", ctypes.c_int64),
+        ("heads", ctypes.c_int32), ("kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+        ("dtype", ctypes.c_int32), ("scale", ctypes.c_float), ("clean_intra", ctypes.c_int32),
+        ("out_f32", ctypes.c_int32),
+    ]
+
+
+class Range(ctypes.Structure):
+    _fields_ = [
+        ("stream", ctypes.c_int32), ("reserved", ctypes.c_int32),
+        ("pos0", ctypes.c_int64), ("len", ctypes.c_int64), ("batch_stride", ctypes.c_int64),
+    ]
+
+    def __init__(self, stream: int, pos0: int, length: int, batch_stride: int = 0):
+        super().__init__(stream, 0, pos0, length, batch_stride)
+
+    def __repr__(self):
+        s = "CLEAN" if self.stream == CLEAN else "CORRUPTED"
+        return f"Range({s}, pos0={self.pos0}, len={self.len}, batch_stride={self.batch_stride})"
+
+
+class BdlmError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"bdlm status {status}: {msg}")
+        self.status = status
+
+
+_LIB = None
+_VP = ctypes.c_void_p
+_PP = ctypes.POINTER(ctypes.c_void_p)
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded HIP library; raises if it has not been built."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(library_path):
+            raise RuntimeError(f"{library_path} is missing: build it first "
+                               "(python -c 'import __graft_entry__ as g; g.build()')")
+        L = ctypes.CDLL(library_path)
+        L.bdlm_last_error.restype = ctypes.c_char_p
+        L.bdlm_attn_fwd.argtypes = [ctypes.POINTER(Problem), ctypes.c_int32, ctypes.POINTER(Range), _PP, _PP, _PP,
+                                    ctypes.c_int32, ctypes.POINTER(Range), _PP, _PP, _VP]
+        L.bdlm_attn_partial_fwd.argtypes = [ctypes.POINTER(Problem), Range, _VP, _VP, _VP, Range, _VP, _VP, _VP]
+        L.bdlm_lse_merge.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                     _PP, _PP, ctypes.c_int32, _VP, _VP, ctypes.c_int32, _VP]
+        L.bdlm_attn_bwd_workspace_bytes.argtypes = [ctypes.POINTER(Problem), ctypes.c_int32, ctypes.POINTER(Range)]
+        L.bdlm_attn_bwd_workspace_bytes.restype = ctypes.c_size_t
+        L.bdlm_attn_bwd.argtypes = [ctypes.POINTER(Problem), ctypes.c_int32, ctypes.POINTER(Range), _PP, _PP, _PP,
+                                    _PP, _PP, ctypes.c_int32, ctypes.POINTER(Range), _PP, _PP, _PP, _PP,
+                                    _VP, ctypes.c_size_t, _VP]
+        L.bdlm_visible_pairs.argtypes = [ctypes.POINTER(Problem), ctypes.c_int32, ctypes.POINTER(Range),
+                                         ctypes.c_int32, ctypes.POINTER(Range)]
+        L.bdlm_visible_pairs.restype = ctypes.c_int64
+        L.bdlm_timing_enable.argtypes = [ctypes.c_int32]
+        L.bdlm_timing_enable.restype = ctypes.c_int
+        L.bdlm_timing_collect.argtypes = [ctypes.c_int32, ctypes.POINTER(ctypes.c_int32), ctypes.POINTER(ctypes.c_float)]
+        L.bdlm_timing_collect.restype = ctypes.c_int32
+        L.bdlm_kernel_name.argtypes = [ctypes.c_int32]
+        L.bdlm_kernel_name.restype = ctypes.c_char_p
+        for name in ("bdlm_attn_fwd", "bdlm_attn_partial_fwd", "bdlm_lse_merge", "bdlm_attn_bwd"):
+            getattr(L, name).restype = ctypes.c_int
+        _LIB = L
+    return _LIB
+
+
+def _check(status: int):
+    if status != 0:
+        raise BdlmError(status, lib().bdlm_last_error().decode())
+
+
+def _ptr(x) -> int:
+    """Device address of a tensor (which must be contiguous and on the GPU) or a raw pointer int."""
+    if x is None:
+        return 0
+    if isinstance(x, int):
+        return x
+    if not x.is_contiguous():
+        raise ValueError(f"tensor of shape {tuple(x.shape)} is not contiguous")
+    if not x.is_cuda:
+        raise ValueError("tensor is not on the GPU")
+    return x.data_ptr()
+
+
+def _parr(xs) -> ctypes.Array:
+    return (ctypes.c_void_p * max(1, len(xs)))(*[_ptr(x) for x in xs])
+
+
+def _rarr(rs: Sequence[Range]) -> ctypes.Array:
+    return (Range * max(1, len(rs)))(*rs)
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _dtype_code(dt: torch.dtype) -> int:
+    if dt == torch.bfloat16:
+        return BF16
+    if dt == torch.float32:
+        return F32
+    raise TypeError(f"unsupported dtype {dt}")
+
+
+def make_problem(batch: int, L: int, block_size: int, heads: int, kv_heads: int, head_dim: int,
+                 dtype, scale: float = 0.0, clean_intra: int = CLEAN_INTRA_CAUSAL, out_f32: bool = False) -> Problem:
+    code = dtype if isinstance(dtype, int) else _dtype_code(dtype)
+    return Problem(batch, L, block_size, heads, kv_heads, head_dim, code, scale, clean_intra, int(bool(out_f32)))
+
+
+def joint_ranges(L: int) -> List[Range]:
+    """The packed ``[x_t ; x]`` layout: corrupted rows [0, L), clean rows [L, 2L) per batch element."""
+    return [Range(CORRUPTED, 0, L, 2 * L), Range(CLEAN, 0, L, 2 * L)]
+
+
+def attn_fwd(p: Problem, q_ranges: Sequence[Range], q, o, lse, k_ranges: Sequence[Range], k, v, stream=None):
+    """``bdlm_attn_fwd``: q/o/lse are lists (one per query range), k/v lists (one per key range)."""
+    _check(lib().bdlm_attn_fwd(ctypes.byref(p), len(q_ranges), _rarr(q_ranges), _parr(q), _parr(o), _parr(lse),
+                               len(k_ranges), _rarr(k_ranges), _parr(k), _parr(v), _stream(stream)))
+
+
+def attn_partial_fwd(p: Problem, qr: Range, q, o, lse, kr: Range, k, v, stream=None):
+    """``bdlm_attn_partial_fwd``: one query range over one key range."""
+    _check(lib().bdlm_attn_partial_fwd(ctypes.byref(p), qr, _ptr(q), _ptr(o), _ptr(lse), kr, _ptr(k), _ptr(v),
+                                       _stream(stream)))
+
+
+def lse_merge(o_parts, lse_parts, o, lse, stream=None):
+    """``bdlm_lse_merge`` of partials shaped ``[batch][rows][heads][d]`` / ``[batch][heads][rows]``."""
+    B, R, H, D = o.shape
+    pdt = _dtype_code(o_parts[0].dtype)
+    _check(lib().bdlm_lse_merge(B, R, H, D, len(o_parts), _parr(o_parts), _parr(lse_parts), pdt,
+                                _ptr(o), _ptr(lse), _dtype_code(o.dtype), _stream(stream)))
+
+
+def attn_bwd_workspace_bytes(p: Problem, q_ranges: Sequence[Range]) -> int:
+    return int(lib().bdlm_attn_bwd_workspace_bytes(ctypes.byref(p), len(q_ranges), _rarr(q_ranges)))
+
+
+def attn_bwd(p: Problem, q_ranges, q, o, lse, dO, dq, k_ranges, k, v, dk, dv, workspace, stream=None):
+    """``bdlm_attn_bwd``; ``workspace`` is a device tensor of at least ``attn_bwd_workspace_bytes`` bytes."""
+    nbytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(lib().bdlm_attn_bwd(ctypes.byref(p), len(q_ranges), _rarr(q_ranges), _parr(q), _parr(o), _parr(lse),
+                               _parr(dO), _parr(dq), len(k_ranges), _rarr(k_ranges), _parr(k), _parr(v),
+                               _parr(dk), _parr(dv), _ptr(workspace), nbytes, _stream(stream)))
+
+
+def visible_pairs(p: Problem, q_ranges: Sequence[Range], k_ranges: Sequence[Range]) -> int:
+    """Valid query-key pairs of the mask per (batch element, query head) (host computation)."""
+    n = lib().bdlm_visible_pairs(ctypes.byref(p), len(q_ranges), _rarr(q_ranges), len(k_ranges), _rarr(k_ranges))
+    if n < 0:
+        raise BdlmError(-1, lib().bdlm_last_error().decode())
+    return int(n)
+
+
+def timing_enable(on: bool = True):
+    """Bracket every kernel this thread enqueues with HIP events (see bdlm_timing_enable)."""
+    _check(lib().bdlm_timing_enable(int(bool(on))))
+
+
+def timing_collect(max_records: int = 1 << 16):
+    """Wait for recorded kernels and return [(kernel_name, ms), ...] in launch order."""
+    ids = (ctypes.c_int32 * max_records)()
+    ms = (ctypes.c_float * max_records)()
+    n = lib().bdlm_timing_collect(max_records, ids, ms)
+    if n < 0:
+        raise BdlmError(n, lib().bdlm_last_error().decode())
+    return [(lib().bdlm_kernel_name(ids[i]).decode(), float(ms[i])) for i in range(n)]
+
+
+# ----------------------------------------------------------- joint helpers
+def _joint_ptrs(t: torch.Tensor, L: int):
+    """Pointers of the corrupted and clean halves of a packed [B][2L][H][D] tensor."""
+    step = L * t.shape[2] * t.shape[3] * t.element_size()
+    return [t.data_ptr(), t.data_ptr() + step]
+
+
+def _check_joint(q, k, v):
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        if not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous device tensor")
+    if q.dim() != 4 or k.shape != v.shape or q.shape[0] != k.shape[0] or q.shape[1] != k.shape[1] \
+            or q.shape[3] != k.shape[3] or q.shape[1] % 2:
+        raise ValueError(f"bad joint shapes q{tuple(q.shape)} k{tuple(k.shape)} v{tuple(v.shape)}")
+
+
+def joint_fwd(q, k, v, block_size: int, clean_intra: int = CLEAN_INTRA_CAUSAL, scale: float = 0.0,
+              out_f32: bool = False, out: Optional[tuple] = None, stream=None):
+    """Fused forward over packed ``[x_t ; x]`` tensors ``q [B][2L][Hq][D]``, ``k, v [B][2L][Hkv][D]``.
+
+    Returns ``(o, lse)`` with ``lse [B][Hq][2L]`` fp32; ``o`` is fp32 when ``out_f32``.
+    """
+    _check_joint(q, k, v)
+    B, n, Hq, D = q.shape
+    L = n // 2
+    p = make_problem(B, L, block_size, Hq, k.shape[2], D, q.dtype, scale, clean_intra, out_f32)
+    odt = torch.float32 if out_f32 else q.dtype
+    o, lse = out if out is not None else (torch.empty(q.shape, dtype=odt, device=q.device),
+                                          torch.empty((B, Hq, n), dtype=torch.float32, device=q.device))
+    r = joint_ranges(L)
+    lp = [lse.data_ptr(), lse.data_ptr() + L * 4]
+    attn_fwd(p, r, _joint_ptrs(q, L), _joint_ptrs(o, L), lp, r, _joint_ptrs(k, L), _joint_ptrs(v, L), stream)
+    return o, lse
+
+
+def joint_bwd(q, k, v, o, lse, do, block_size: int, clean_intra: int = CLEAN_INTRA_CAUSAL, scale: float = 0.0,
+              out_f32: bool = False, out: Optional[tuple] = None, workspace: Optional[torch.Tensor] = None,
+              stream=None):
+    """Backward of :func:`joint_fwd`; returns ``(dq, dk, dv)`` (fp32 when ``out_f32``; ``o`` must match)."""
+    _check_joint(q, k, v)
+    B, n, Hq, D = q.shape
+    L = n // 2
+    p = make_problem(B, L, block_size, Hq, k.shape[2], D, q.dtype, scale, clean_intra, out_f32)
+    r = joint_ranges(L)
+    odt = torch.float32 if out_f32 else q.dtype
+    if o.dtype != odt:
+        raise TypeError(f"o must be {odt}")
+    if out is None:
+        out = tuple(torch.empty(t.shape, dtype=odt, device=q.device) for t in (q, k, v))
+    dq, dk, dv = out
+    if workspace is None:
+        workspace = torch.empty(attn_bwd_workspace_bytes(p, r), dtype=torch.uint8, device=q.device)
+    lp = [lse.data_ptr(), lse.data_ptr() + L * 4]
+    attn_bwd(p, r, _joint_ptrs(q, L), _joint_ptrs(o, L), lp, _joint_ptrs(do, L), _joint_ptrs(dq, L),
+             r, _joint_ptrs(k, L), _joint_ptrs(v, L), _joint_ptrs(dk, L), _joint_ptrs(dv, L), workspace, stream)
+    return dq, dk, dv
+
+
+def useful_flops(pairs_per_head: int, heads: int, batch: int, head_dim: int) -> dict:
+    """Useful FLOPs of the valid pairs: 4 d per pair forward (Q K^T, P V), 10 d backward (five products)."""
+    n = pairs_per_head * heads * batch
+    return {"fwd": 4 * head_dim * n, "bwd": 10 * head_dim * n, "total": 14 * head_dim * n}
+
+
+def default_scale(head_dim: int) -> float:
+    return 1.0 / math.sqrt(head_dim)

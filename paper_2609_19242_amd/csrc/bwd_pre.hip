@@ -1,0 +1,132 @@
+// Backward pre- and post-processing, gfx950 (HBM-bound elementwise passes).
+//
+// pre:  D[b][h][row] = sum_d dO * O in fp32 (the row dot the softmax gradient
+//       dS = P * (dP - D) needs; arXiv 2609.19242 App. C reuses the saved O)
+//       and, for the bf16 path, zero the fp32 dQ accumulator.
+// post: dQ = bf16(scale * accumulator).
+// One thread per 8 consecutive head_dim elements; the D/8 threads of one
+// (row, head) are adjacent lanes and reduce with cross-lane shuffles.
+#include "common.hpp"
+#include "device.hpp"
+
+namespace bdlm {
+
+namespace {
+
+template <int D, typename T, typename TO>
+__global__ __launch_bounds__(256) void bwd_pre_kernel(const AttnArgs a, int zero_acc) {
+  constexpr int CPR = D / 8;
+  const QRangeArg& qr = a.qr[blockIdx.y];
+  const int64_t H = a.heads;
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t total = (int64_t)a.batch * qr.len * H * CPR;
+  const bool ok = gid < total;
+  const int64_t g = ok ? gid : 0;
+  const int chunk = (int)(g % CPR);
+  const int64_t rh = g / CPR;  // (b * len + row) * H + h
+  const int h = (int)(rh % H);
+  const int64_t brow = rh / H;
+  const int64_t row = brow % qr.len, b = brow / qr.len;
+  const int64_t off = ((b * qr.bstride + row) * H + h) * D + chunk * 8;
+  float s = 0.f;
+  if (ok) {
+    float o[8], d[8];
+    if constexpr (sizeof(TO) == 2) {
+      const bf16x8 x = *(const bf16x8*)((const bf16*)qr.o + off);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = (float)x[e];
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = ((const float*)qr.o)[off + e];
+    }
+    if constexpr (sizeof(T) == 2) {
+      const bf16x8 x = *(const bf16x8*)((const bf16*)qr.dO + off);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) d[e] = (float)x[e];
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) d[e] = ((const float*)qr.dO)[off + e];
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) s = fmaf(o[e], d[e], s);
+  }
+#pragma unroll
+  for (int w = CPR / 2; w > 0; w >>= 1) s += __shfl_xor(s, w, CPR);
+  if (!ok) return;
+  if (chunk == 0) qr.delta[(b * H + h) * qr.len + row] = s;
+  if (zero_acc) {
+    f32x4 z = {0.f, 0.f, 0.f, 0.f};
+    f32x4* p = (f32x4*)(qr.dqacc + rh * D + chunk * 8);
+    p[0] = z;
+    p[1] = z;
+  }
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void bwd_post_kernel(const AttnArgs a) {
+  constexpr int CPR = D / 8;
+  const QRangeArg& qr = a.qr[blockIdx.y];
+  const int64_t H = a.heads;
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (gid >= (int64_t)a.batch * qr.len * H * CPR) return;
+  const int chunk = (int)(gid % CPR);
+  const int64_t rh = gid / CPR;
+  const int64_t h = rh % H, brow = rh / H;
+  const int64_t row = brow % qr.len, b = brow / qr.len;
+  const f32x4* src = (const f32x4*)(qr.dqacc + rh * D + chunk * 8);
+  const f32x4 x0 = src[0], x1 = src[1];
+  const int64_t dst = ((b * qr.bstride + row) * H + h) * D + chunk * 8;
+  if (a.out_f32) {
+    f32x4* y = (f32x4*)((float*)qr.dq + dst);
+    y[0] = x0 * a.scale;
+    y[1] = x1 * a.scale;
+  } else {
+    bf16x8 y;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      y[e] = to_bf16(x0[e] * a.scale);
+      y[4 + e] = to_bf16(x1[e] * a.scale);
+    }
+    *(bf16x8*)((bf16*)qr.dq + dst) = y;
+  }
+}
+
+int64_t max_q_threads(const AttnArgs& a, int cpr) {
+  int64_t m = 0;
+  for (int i = 0; i < a.n_q; ++i) {
+    const int64_t t = (int64_t)a.batch * a.qr[i].len * a.heads * cpr;
+    m = t > m ? t : m;
+  }
+  return m;
+}
+
+}  // namespace
+
+hipError_t launch_bwd_pre(const AttnArgs& a, int head_dim, int dtype, hipStream_t s) {
+  const int64_t t = max_q_threads(a, head_dim / 8);
+  if (t == 0) return hipSuccess;
+  const dim3 grid((unsigned)((t + 255) / 256), a.n_q);
+  const int zero = dtype == 0;
+  if (dtype == 0 && !a.out_f32) {
+    if (head_dim == 128) hipLaunchKernelGGL((bwd_pre_kernel<128, bf16, bf16>), grid, dim3(256), 0, s, a, zero);
+    else hipLaunchKernelGGL((bwd_pre_kernel<64, bf16, bf16>), grid, dim3(256), 0, s, a, zero);
+  } else if (dtype == 0) {
+    if (head_dim == 128) hipLaunchKernelGGL((bwd_pre_kernel<128, bf16, float>), grid, dim3(256), 0, s, a, zero);
+    else hipLaunchKernelGGL((bwd_pre_kernel<64, bf16, float>), grid, dim3(256), 0, s, a, zero);
+  } else {
+    if (head_dim == 128) hipLaunchKernelGGL((bwd_pre_kernel<128, float, float>), grid, dim3(256), 0, s, a, zero);
+    else hipLaunchKernelGGL((bwd_pre_kernel<64, float, float>), grid, dim3(256), 0, s, a, zero);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_post_bf16(const AttnArgs& a, int head_dim, hipStream_t s) {
+  const int64_t t = max_q_threads(a, head_dim / 8);
+  if (t == 0) return hipSuccess;
+  const dim3 grid((unsigned)((t + 255) / 256), a.n_q);
+  if (head_dim == 128) hipLaunchKernelGGL((bwd_post_kernel<128>), grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL((bwd_post_kernel<64>), grid, dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace bdlm

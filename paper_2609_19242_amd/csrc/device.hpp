@@ -1,0 +1,66 @@
+// gfx950 device helpers: vector types, MFMA, buffer loads, LDS transpose reads.
+//
+// Lane layouts (checked on the GPU):
+//  * v_mfma_f32_32x32x16_bf16 -- A (32x16): lane l holds row l%32, k = 8*(l/32)+j;
+//    B (16x32): lane l holds column l%32, k = 8*(l/32)+j;  C (32x32): lane l,
+//    register i holds column l%32, row 8*(i/4) + 4*(l/32) + i%4.
+//  * ds_read_b64_tr_b16 -- inside each group of 16 lanes, lane i receives
+//    element i%4 of the 8-byte rows addressed by lanes i/4, i/4+4, i/4+8,
+//    i/4+12.  Addressing row R(s/4), column c0 + 4*(s%4) from source lane s
+//    therefore hands lane i the column c0 + i of rows R(0..3): a transposed
+//    4x16 fragment, which is how row-major V, Q and dO tiles in LDS become the
+//    k-major MFMA operands the products P V, dO^T P and Q^T dS need.
+//  * v_permlane32_swap with both operands x: result[0] holds x of lanes 0..31
+//    in both halves, result[1] holds x of lanes 32..63 in both halves.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace bdlm {
+
+typedef __bf16 bf16;
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4;
+typedef short short4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// Raw buffer resource over [base, base + bytes): loads past the end return zero.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+__device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 0));
+}
+
+// Transposed 8-byte LDS read (see the header comment).  p must point into LDS.
+__device__ __forceinline__ bf16x4 lds_read_tr(const bf16* p) {
+  typedef __attribute__((address_space(3))) short4_t lds_s4;
+  typedef __attribute__((address_space(3))) bf16 lds_bf16;
+  short4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4*)(lds_bf16*)p);
+  return __builtin_bit_cast(bf16x4, v);
+}
+
+__device__ __forceinline__ bf16x8 cat(bf16x4 a, bf16x4 b) {
+  return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// x of the lane l ^ 32 (the other half of the wavefront).
+__device__ __forceinline__ float partner(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  const uint32_t lane = __lane_id();
+  return __uint_as_float(lane < 32 ? r[1] : r[0]);
+}
+
+__device__ __forceinline__ float exp2f_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+
+__device__ __forceinline__ bf16 to_bf16(float x) { return (bf16)x; }
+
+}  // namespace bdlm

@@ -1,0 +1,142 @@
+"""Host-side checks of the C ABI: the library loads, exports every declared
+symbol, rejects invalid arguments before any launch, and its pair counter
+matches the paper's closed form and the oracle's explicit mask.
+
+No GPU is touched: every call here fails validation (returns before any HIP
+call) or is host-only (bdlm_visible_pairs, bdlm_attn_bwd_workspace_bytes).
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+import oracle
+import paper_2609_19242_amd as bd
+from paper_2609_19242_amd import CLEAN, CORRUPTED, Range
+from synth import WORKLOADS
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "bdlm_attn.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(bd.library_path), reason="library not built")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(bdlm_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert {"bdlm_attn_fwd", "bdlm_attn_bwd", "bdlm_attn_partial_fwd", "bdlm_lse_merge"} <= set(names)
+    L = bd.lib()
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def _prob(**kw):
+    base = dict(batch=1, L=64, block_size=16, heads=4, kv_heads=2, head_dim=128, dtype=bd.BF16)
+    base.update(kw)
+    return bd.make_problem(**base)
+
+
+FAKE = 0x10000  # never dereferenced: these calls fail validation first
+
+
+def _fwd(p, qr=None, kr=None, ptr=FAKE):
+    qr = qr or [Range(CORRUPTED, 0, p.L)]
+    kr = kr or [Range(CLEAN, 0, p.L)]
+    return bd.lib().bdlm_attn_fwd(ctypes.byref(p), len(qr), bd._rarr(qr), bd._parr([ptr] * len(qr)),
+                                  bd._parr([ptr] * len(qr)), bd._parr([ptr] * len(qr)), len(kr), bd._rarr(kr),
+                                  bd._parr([ptr] * len(kr)), bd._parr([ptr] * len(kr)), None)
+
+
+@pytest.mark.parametrize("kw,status,needle", [
+    (dict(L=60, block_size=16), -1, "block_size"),
+    (dict(heads=3, kv_heads=2), -1, "kv_heads"),
+    (dict(head_dim=96), -2, "head_dim"),
+    (dict(dtype=7), -2, "dtype"),
+    (dict(batch=0), -1, "batch"),
+    (dict(clean_intra=5), -1, "clean_intra"),
+])
+def test_invalid_problem_rejected(kw, status, needle):
+    assert _fwd(_prob(**kw)) == status
+    assert needle in bd.lib().bdlm_last_error().decode()
+
+
+def test_invalid_ranges_rejected():
+    p = _prob()
+    assert _fwd(p, qr=[Range(CORRUPTED, 60, 8)]) == -1  # past L
+    assert "outside" in bd.lib().bdlm_last_error().decode()
+    assert _fwd(p, qr=[Range(2, 0, 8)]) == -1  # bad stream
+    assert _fwd(p, qr=[Range(CLEAN, 0, 8, 4)]) == -1  # batch_stride < len
+    assert _fwd(p, kr=[Range(CLEAN, 0, 8)] * 33) == -2  # too many key ranges
+    assert _fwd(p, ptr=FAKE + 8) == -1  # misaligned
+    assert "aligned" in bd.lib().bdlm_last_error().decode()
+    assert _fwd(p, ptr=0) == -1  # null
+    L = bd.lib()
+    assert L.bdlm_attn_fwd(ctypes.byref(p), 0, None, None, None, None, 1, bd._rarr([Range(CLEAN, 0, 8)]),
+                           None, None, None) == -1
+
+
+def test_merge_and_bwd_validation():
+    L = bd.lib()
+    parts = bd._parr([FAKE])
+    assert L.bdlm_lse_merge(1, 8, 2, 128, 0, parts, parts, 0, FAKE, FAKE, 0, None) == -1
+    assert L.bdlm_lse_merge(1, 8, 2, 128, 33, parts, parts, 0, FAKE, FAKE, 0, None) == -2
+    assert L.bdlm_lse_merge(1, 8, 2, 80, 1, parts, parts, 0, FAKE, FAKE, 0, None) == -2
+    assert L.bdlm_lse_merge(1, 8, 2, 128, 1, parts, parts, 0, FAKE, FAKE + 64, 0, None) == -1  # o aliases a part
+    p = _prob()
+    qr = [Range(CORRUPTED, 0, 64)]
+    need = bd.attn_bwd_workspace_bytes(p, qr)
+    assert need == 256 * (-(-64 * 4 * 128 * 4 // 256)) + 256 * (-(-64 * 4 * 4 // 256))
+    f = bd._parr([FAKE])
+    rc = L.bdlm_attn_bwd(ctypes.byref(p), 1, bd._rarr(qr), f, f, f, f, f, 1, bd._rarr([Range(CLEAN, 0, 64)]),
+                         f, f, f, f, FAKE, need - 1, None)
+    assert rc == -4 and "workspace" in L.bdlm_last_error().decode()
+
+
+# ------------------------------------------------------------ pair counter
+def golden_pairs():
+    out = {}
+    with open(os.path.join(ROOT, "tests", "golden", "pair_counts.txt")) as f:
+        for line in f:
+            if line.startswith("#") or not line.strip():
+                continue
+            name, Lf, Mf, reading, pairs = line.split()
+            out[(name, Lf, Mf, reading)] = int(pairs)
+    return out
+
+
+@pytest.mark.parametrize("name", ["tiny", "4k", "32k", "128k"])
+@pytest.mark.parametrize("reading", ["causal", "block"])
+def test_visible_pairs_match_closed_form(name, reading):
+    w = WORKLOADS[name]
+    rd = bd.CLEAN_INTRA_CAUSAL if reading == "causal" else bd.CLEAN_INTRA_BLOCK
+    p = bd.make_problem(w.batch, w.L, w.block_size, w.heads, w.kv_heads, w.head_dim, bd.BF16, 0.0, rd)
+    r = bd.joint_ranges(w.L)
+    want = golden_pairs()[(name, f"L={w.L}", f"M={w.block_size}", reading)]
+    assert bd.visible_pairs(p, r, r) == want
+
+
+def test_visible_pairs_csbp_rank():
+    w = WORKLOADS["csbp256k"]
+    p = bd.make_problem(1, w.L, w.block_size, w.heads, w.kv_heads, w.head_dim, bd.BF16)
+    qr = [Range(CORRUPTED, w.local_pos0, w.local_tokens)]
+    kr = [Range(CORRUPTED, w.local_pos0, w.local_tokens)] + \
+         [Range(CLEAN, s * w.shard_tokens, w.shard_tokens) for s in range(w.n_shards)]
+    assert bd.visible_pairs(p, qr, kr) == 2281963520
+
+
+@pytest.mark.parametrize("L,M", [(24, 4), (40, 8), (17, 17), (12, 1)])
+@pytest.mark.parametrize("reading", [0, 1])
+def test_visible_pairs_match_oracle_popcount(L, M, reading):
+    p = bd.make_problem(1, L, M, 1, 1, 64, bd.BF16, 0.0, reading)
+    qr = [Range(CORRUPTED, 0, L), Range(CLEAN, 0, L)]
+    kr = [Range(CORRUPTED, 0, L), Range(CLEAN, 3, L - 5), Range(CLEAN, 0, 3)]
+    got = bd.visible_pairs(p, qr, kr)
+    want = oracle.count_visible_pairs([(CORRUPTED, 0, L), (CLEAN, 0, L)],
+                                      [(CORRUPTED, 0, L), (CLEAN, 3, L - 5), (CLEAN, 0, 3)], M, reading)
+    assert got == want

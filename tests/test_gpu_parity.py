@@ -1,0 +1,219 @@
+"""GPU parity: the HIP library (through its C ABI) against the fp64 oracle.
+
+Small shapes span several tiles and ragged tails in every dimension the
+kernels tile (256-row forward query tiles, 64-key forward key tiles, 128-key
+backward key tiles, 32-row backward query steps); they cover both readings of
+the clean-to-clean rule, GQA groups, head_dim 64 and 128, batch > 1, the
+degenerate block sizes (1 and L) and rows that see no key.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_19242_amd as bd
+from paper_2609_19242_amd import CLEAN, CORRUPTED, Range
+from synth import WORKLOADS, make_joint
+from tests.gpu_util import assert_close, assert_close_bf16_out, joint_inputs, kv_group_heads
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def run_joint(q, k, v, do, M, reading, out_f32):
+    qd, kd, vd, dod = (t.to(DEV) for t in (q, k, v, do))
+    o, lse = bd.joint_fwd(qd, kd, vd, M, clean_intra=reading, out_f32=out_f32)
+    dq, dk, dv = bd.joint_bwd(qd, kd, vd, o, lse, dod, M, clean_intra=reading, out_f32=out_f32)
+    torch.cuda.synchronize()
+    return o, lse, dq, dk, dv
+
+
+def check_joint(q, k, v, do, M, reading, dtype, heads=None, tag="", out_f32=True):
+    """GPU joint fwd+bwd against the oracle on the query heads ``heads`` (all by default).
+
+    Strict tolerance on fp32 outputs; with bf16 outputs (``out_f32=False``) the
+    bound adds the output rounding.
+    """
+    L = q.shape[1] // 2
+    o, lse, dq, dk, dv = run_joint(q, k, v, do, M, reading, out_f32)
+    hs = list(range(q.shape[2])) if heads is None else heads
+    O, LSE = oracle.joint_fwd(q, k, v, L, M, clean_intra=reading, heads=hs)
+    dQ, dK, dV = oracle.joint_bwd(q, k, v, O, LSE, do[:, :, hs], L, M, clean_intra=reading, heads=hs)
+    kvs = sorted(set(h // (q.shape[2] // k.shape[2]) for h in hs))
+    assert_close(f"{tag} LSE", lse[:, hs], LSE, dtype)
+    pairs = (("O", o[:, :, hs], O), ("dQ", dq[:, :, hs], dQ), ("dK", dk[:, :, kvs], dK[:, :, kvs]),
+             ("dV", dv[:, :, kvs], dV[:, :, kvs]))
+    for name, got, ref in pairs:
+        if out_f32 or dtype == torch.float32:
+            assert_close(f"{tag} {name}", got, ref, dtype)
+        else:
+            assert_close_bf16_out(f"{tag} {name}", got, ref)
+    return o, lse, dq, dk, dv
+
+
+SMALL = [
+    # L, M, Hq, Hkv, D, batch
+    (300, 12, 4, 2, 128, 1),
+    (300, 20, 2, 2, 64, 2),
+    (320, 1, 4, 1, 128, 1),
+    (256, 256, 2, 1, 128, 1),
+    (200, 8, 8, 2, 128, 1),
+    (520, 40, 2, 1, 128, 1),
+]
+
+
+@pytest.mark.parametrize("mode", ["bf16", "bf16-out-bf16", "fp32"])
+@pytest.mark.parametrize("reading", [0, 1], ids=["causal", "block"])
+@pytest.mark.parametrize("shape", SMALL, ids=lambda s: "L{}-M{}-H{}x{}-d{}-b{}".format(*s))
+def test_joint_small(shape, reading, mode):
+    L, M, Hq, Hkv, D, B = shape
+    dtype = torch.float32 if mode == "fp32" else torch.bfloat16
+    q, k, v, do = joint_inputs(L, Hq, Hkv, D, dtype, batch=B, seed=L + M + D)
+    check_joint(q, k, v, do, M, reading, dtype, tag=f"L{L} M{M} r{reading}", out_f32=(mode != "bf16-out-bf16"))
+
+
+@pytest.mark.parametrize("reading", [0, 1], ids=["causal", "block"])
+def test_workload_tiny_fp32(reading):
+    w = WORKLOADS["tiny"]
+    q, k, v, do = make_joint(w)
+    check_joint(q, k, v, do, w.block_size, reading, torch.float32, tag=f"tiny r{reading}")
+
+
+def test_workload_4k_bf16_head_subset():
+    w = WORKLOADS["4k"]
+    q, k, v, do = make_joint(w)
+    hs = kv_group_heads(w.heads, w.kv_heads, [0, w.kv_heads - 1])
+    o, lse, *_ = check_joint(q, k, v, do, w.block_size, 0, torch.bfloat16, heads=hs, tag="4k")
+    assert torch.isfinite(o).all() and torch.isfinite(lse).all()
+
+
+# ------------------------------------------------------ partial + merge, CSBP
+def csbp_case(dtype, M=8, n_local=96, pos0=512, shard=256, n_shards=4, Hq=4, Hkv=2, D=128, seed=5):
+    import synth
+    q = synth.normal((1, n_local, Hq, D), seed, dtype)
+    kl = synth.normal((1, n_local, Hkv, D), seed + 1, dtype)
+    vl = synth.normal((1, n_local, Hkv, D), seed + 2, dtype)
+    kc = synth.normal((1, shard * n_shards, Hkv, D), seed + 3, dtype)
+    vc = synth.normal((1, shard * n_shards, Hkv, D), seed + 4, dtype)
+    do = synth.normal((1, n_local, Hq, D), seed + 5, dtype)
+    qr = Range(CORRUPTED, pos0, n_local)
+    krs = [Range(CORRUPTED, pos0, n_local)] + [Range(CLEAN, s * shard, shard) for s in range(n_shards)]
+    ks = [kl] + [kc[:, s * shard:(s + 1) * shard].contiguous() for s in range(n_shards)]
+    vs = [vl] + [vc[:, s * shard:(s + 1) * shard].contiguous() for s in range(n_shards)]
+    return q, ks, vs, do, qr, krs
+
+
+@pytest.mark.parametrize("mode", ["bf16", "bf16-out-bf16", "fp32"])
+def test_csbp_partials_merge_and_backward(mode):
+    M = 8
+    dtype = torch.float32 if mode == "fp32" else torch.bfloat16
+    out_f32 = mode != "bf16-out-bf16"
+    odt = torch.float32 if out_f32 else dtype
+    q, ks, vs, do, qr, krs = csbp_case(dtype, M=M)
+    B, n, Hq, D = q.shape
+    Hkv = ks[0].shape[2]
+    L = 2048
+    p = bd.make_problem(1, L, M, Hq, Hkv, D, dtype, out_f32=out_f32)
+    qd, dod = q.to(DEV), do.to(DEV)
+    kd = [t.to(DEV) for t in ks]
+    vd = [t.to(DEV) for t in vs]
+    o_parts, l_parts = [], []
+    for kr, kk, vv in zip(krs, kd, vd):
+        o = torch.empty(qd.shape, dtype=odt, device=DEV)
+        lse = torch.empty((1, Hq, n), dtype=torch.float32, device=DEV)
+        bd.attn_partial_fwd(p, qr, qd, o, lse, kr, kk, vv)
+        o_parts.append(o)
+        l_parts.append(lse)
+    om = torch.empty(qd.shape, dtype=odt, device=DEV)
+    lm = torch.empty((1, Hq, n), dtype=torch.float32, device=DEV)
+    bd.lse_merge(o_parts, l_parts, om, lm)
+    # fused multi-range forward in one launch
+    of = torch.empty(qd.shape, dtype=odt, device=DEV)
+    lf = torch.empty((1, Hq, n), dtype=torch.float32, device=DEV)
+    bd.attn_fwd(p, [qr], [qd], [of], [lf], krs, kd, vd)
+    torch.cuda.synchronize()
+
+    qranges = [(CORRUPTED, qr.pos0, qr.len)]
+    kranges = [(r.stream, r.pos0, r.len) for r in krs]
+    kall = torch.cat(ks, dim=1)
+    vall = torch.cat(vs, dim=1)
+    O, LSE = oracle.fwd(q, kall, vall, qranges, kranges, M)
+    def close(name, got, ref):
+        if out_f32:
+            assert_close(name, got, ref, dtype)
+        else:
+            assert_close_bf16_out(name, got, ref)
+
+    for j, (kr, kk, vv) in enumerate(zip(krs, ks, vs)):
+        Oj, Lj = oracle.fwd(q, kk, vv, qranges, [kranges[j]], M)
+        close(f"partial{j} O", o_parts[j], Oj)
+        assert_close(f"partial{j} LSE", l_parts[j], Lj, dtype)
+    # shard 3 covers clean positions 768..1023, beyond every local block's prefix
+    assert torch.isneginf(l_parts[4]).all() and (o_parts[4] == 0).all()
+    close("merged O", om, O)
+    assert_close("merged LSE", lm, LSE, dtype)
+    close("fused O", of, O)
+    assert_close("fused LSE", lf, LSE, dtype)
+
+    # backward over the key-range list with the merged (O, LSE)
+    dq = torch.empty(qd.shape, dtype=odt, device=DEV)
+    dks = [torch.empty(t.shape, dtype=odt, device=DEV) for t in kd]
+    dvs = [torch.empty(t.shape, dtype=odt, device=DEV) for t in vd]
+    ws = torch.empty(bd.attn_bwd_workspace_bytes(p, [qr]), dtype=torch.uint8, device=DEV)
+    bd.attn_bwd(p, [qr], [qd], [om], [lm], [dod], [dq], krs, kd, vd, dks, dvs, ws)
+    torch.cuda.synchronize()
+    dQ, dK, dV = oracle.bwd(q, kall, vall, O, LSE, do, qranges, kranges, M)
+    close("csbp dQ", dq, dQ)
+    off = 0
+    for j, kk in enumerate(ks):
+        nrows = kk.shape[1]
+        close(f"csbp dK{j}", dks[j], dK[:, off:off + nrows])
+        close(f"csbp dV{j}", dvs[j], dV[:, off:off + nrows])
+        off += nrows
+    assert (dks[4] == 0).all() and (dvs[4] == 0).all()
+
+
+def test_merge_kernel_random_partials():
+    """Merge of arbitrary partials (including all-empty rows) against the oracle's merge."""
+    g = torch.Generator().manual_seed(3)
+    B, R, H, D, J = 2, 77, 3, 128, 5
+    os_ = [torch.randn(B, R, H, D, generator=g) for _ in range(J)]
+    ls = [torch.randn(B, H, R, generator=g) * 4 for _ in range(J)]
+    for j in range(J):  # some parts empty for some rows
+        mask = torch.rand(B, H, R, generator=g) < 0.3
+        ls[j][mask] = -float("inf")
+    ls[0][:, :, :5] = -float("inf")
+    for j in range(1, J):
+        ls[j][:, :, :5] = -float("inf")
+    for j in range(J):
+        os_[j] = torch.where(torch.isneginf(ls[j]).transpose(1, 2)[..., None], torch.zeros(()), os_[j]).contiguous()
+    O, LSE = oracle.lse_merge(os_, ls)
+    for pdt, odt in ((torch.float32, torch.float32), (torch.bfloat16, torch.bfloat16), (torch.bfloat16, torch.float32)):
+        od = [t.to(pdt).to(DEV) for t in os_]
+        ld = [t.to(DEV) for t in ls]
+        o = torch.empty(B, R, H, D, dtype=odt, device=DEV)
+        lse = torch.empty(B, H, R, dtype=torch.float32, device=DEV)
+        bd.lse_merge(od, ld, o, lse)
+        torch.cuda.synchronize()
+        Or, Lr = oracle.lse_merge([t.to(pdt) for t in os_], ls)
+        tol = torch.float32 if (pdt, odt) == (torch.float32, torch.float32) else torch.bfloat16
+        assert_close(f"merge {pdt}->{odt} O", o, Or, tol)
+        assert_close(f"merge {pdt}->{odt} LSE", lse, Lr, tol)
+        assert (o[:, :5] == 0).all() and torch.isneginf(lse[:, :, :5]).all()
+
+
+def test_empty_rows_partial():
+    """Corrupted queries of block 0 over the clean stream: O = 0 exactly, LSE = -inf."""
+    L, M, H, D = 256, 32, 2, 128
+    q, k, v, _ = joint_inputs(L, H, H, D, torch.bfloat16, seed=9)
+    p = bd.make_problem(1, L, M, H, H, D, torch.bfloat16)
+    qd = q[:, :L].contiguous().to(DEV)
+    kd, vd = k[:, L:].contiguous().to(DEV), v[:, L:].contiguous().to(DEV)
+    o = torch.full(qd.shape, 7.0, dtype=torch.bfloat16, device=DEV)
+    lse = torch.zeros((1, H, L), dtype=torch.float32, device=DEV)
+    bd.attn_partial_fwd(p, Range(CORRUPTED, 0, L), qd, o, lse, Range(CLEAN, 0, L), kd, vd)
+    torch.cuda.synchronize()
+    assert (o[:, :M] == 0).all() and torch.isneginf(lse[:, :, :M]).all()
+    O, LSE = oracle.fwd(q[:, :L], k[:, L:], v[:, L:], [(CORRUPTED, 0, L)], [(CLEAN, 0, L)], M)
+    assert_close("empty-rows O", o, O, torch.bfloat16)
+    assert_close("empty-rows LSE", lse, LSE, torch.bfloat16)

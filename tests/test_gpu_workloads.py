@@ -1,0 +1,206 @@
+"""GPU parity at the full workload sizes (32K joint, one 256K CSBP rank, 128K joint).
+
+The GPU computes every head and row in the launch configuration bench.py
+times.  The fp64 oracle checks, on the query heads of KV groups {0, last}:
+
+* sampled query rows (block edges of both streams and seeded random rows):
+  O, LSE and dQ -- each needs only its own row's keys;
+* every key row whose visible queries are few enough to enumerate: the
+  corrupted keys of sampled blocks (seen only by their own block's queries,
+  eq:correctness-block-dependency) and the clean keys of the last two blocks:
+  dK and dV complete;
+* for all keys of every KV head, the identity sum_j dV_j = sum_i dO_i over the
+  group's heads (softmax rows sum to one), which catches any lost or doubled
+  key tile at any size.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_19242_amd as bd
+import synth
+from paper_2609_19242_amd import CLEAN, CORRUPTED, Range
+from synth import WORKLOADS
+from tests.gpu_util import assert_close, kv_group_heads
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+F32 = torch.float32
+BF16 = torch.bfloat16  # tolerance class of these runs: bf16 inputs, fp32 accumulation, fp32 outputs
+
+
+def sample_rows(L, M, n_random, seed):
+    corr = [0, M - 1, M, L // 2, L - M, L - 1]
+    clean = [L + x for x in (0, 1, M - 1, M, L // 2, L - 1)]
+    rng = np.random.default_rng(seed)
+    rnd = rng.choice(2 * L, size=n_random, replace=False).tolist()
+    return sorted(set(corr + clean + rnd))
+
+
+def to_cpu_heads(t, heads):
+    return t[:, :, heads].cpu()
+
+
+def dv_identity(dv, do, group, tag):
+    """sum over all key rows of dV equals sum over all query rows of dO (per batch, KV head)."""
+    B, _, Hkv, D = dv.shape
+    lhs = dv.double().sum(dim=1)  # [B][Hkv][D]
+    rhs = do.double().sum(dim=1).reshape(B, Hkv, group, D).sum(dim=2)
+    err = float((lhs - rhs).norm() / rhs.norm())
+    print(f"{tag} sum dV identity rel_l2={err:.3e}", flush=True)
+    assert err < 5e-3, err
+
+
+def joint_check(w, reading=0, n_random=24):
+    L, M = w.L, w.block_size
+    torch.cuda.empty_cache()
+    q, k, v, do = synth.make_joint(w, device=DEV)
+    o, lse = bd.joint_fwd(q, k, v, M, clean_intra=reading, out_f32=True)
+    dq, dk, dv = bd.joint_bwd(q, k, v, o, lse, do, M, clean_intra=reading, out_f32=True)
+    torch.cuda.synchronize()
+    tag = w.name
+    assert torch.isfinite(o).all() and torch.isfinite(lse).all()
+    assert torch.isfinite(dq).all() and torch.isfinite(dk).all() and torch.isfinite(dv).all()
+    dv_identity(dv, do, w.heads // w.kv_heads, tag)
+
+    kvs = [0, w.kv_heads - 1]
+    hs = kv_group_heads(w.heads, w.kv_heads, kvs)
+    g = w.heads // w.kv_heads
+    qc, doc = to_cpu_heads(q, hs), to_cpu_heads(do, hs)  # bf16 on the host; rows are picked before upcasting
+    kc, vc = k[:, :, kvs].cpu(), v[:, :, kvs].cpu()
+    # the oracle sees the sampled heads renumbered 0..len(hs)-1 over KV heads 0..len(kvs)-1
+    r = oracle.joint_ranges(L)
+    s_all, p_all = oracle.rows_of(r)
+
+    # ---- sampled query rows: O, LSE, dQ
+    rows = sample_rows(L, M, n_random, seed=w.index)
+    single = [(int(s_all[i]), int(p_all[i]), 1) for i in rows]
+    O, LSE = oracle.fwd(qc[:, rows], kc, vc, single, r, M, clean_intra=reading, chunk=128)
+    assert_close(f"{tag} O rows", o[:, rows][:, :, hs], O, BF16)
+    assert_close(f"{tag} LSE rows", lse[:, hs][:, :, rows], LSE, BF16)
+    dQ, _, _ = oracle.bwd(qc[:, rows], kc, vc, O, LSE, doc[:, rows], single, r, M, clean_intra=reading, chunk=128)
+    assert_close(f"{tag} dQ rows", dq[:, rows][:, :, hs], dQ, BF16)
+
+    # ---- key rows with few visible queries: corrupted blocks and the last two clean blocks
+    nb = L // M
+    key_sets = []
+    for blk in (0, 1, nb // 2, nb - 1):
+        qrows = list(range(blk * M, (blk + 1) * M))
+        key_sets.append((f"corrupted block {blk}", qrows, list(range(blk * M, (blk + 1) * M))))
+    qrows = list(range(2 * L - 2 * M, 2 * L)) + list(range(L - M, L))
+    key_sets.append(("last clean blocks", qrows, list(range(2 * L - 2 * M, 2 * L))))
+    for name, qrows, krows in key_sets:
+        single = [(int(s_all[i]), int(p_all[i]), 1) for i in qrows]
+        Oq, Lq = oracle.fwd(qc[:, qrows], kc, vc, single, r, M, clean_intra=reading, chunk=128)
+        _, dK, dV = oracle.bwd(qc[:, qrows], kc, vc, Oq, Lq, doc[:, qrows], single, r, M, clean_intra=reading,
+                               chunk=128)
+        assert_close(f"{tag} dK {name}", dk[:, krows][:, :, kvs], dK[:, krows], BF16)
+        assert_close(f"{tag} dV {name}", dv[:, krows][:, :, kvs], dV[:, krows], BF16)
+    del q, k, v, do, o, lse, dq, dk, dv
+    torch.cuda.empty_cache()
+
+
+def test_workload_32k_causal():
+    joint_check(WORKLOADS["32k"], 0)
+
+
+def test_workload_32k_block_reading():
+    joint_check(WORKLOADS["32k"], 1, n_random=8)
+
+
+def test_workload_128k():
+    joint_check(WORKLOADS["128k"], 0, n_random=8)
+
+
+def csbp_ranges(w):
+    qr = Range(CORRUPTED, w.local_pos0, w.local_tokens)
+    krs = [Range(CORRUPTED, w.local_pos0, w.local_tokens)] + \
+          [Range(CLEAN, s * w.shard_tokens, w.shard_tokens) for s in range(w.n_shards)]
+    return qr, krs
+
+
+def shard_views(t, w):
+    """Pointers of the shards of a contiguous clean-prefix buffer [1][clean][Hkv][D]."""
+    step = w.shard_tokens * t.shape[2] * t.shape[3] * t.element_size()
+    return [t.data_ptr() + s * step for s in range(w.n_shards)]
+
+
+def test_workload_csbp256k():
+    w = WORKLOADS["csbp256k"]
+    torch.cuda.empty_cache()
+    q, kl, vl, kc, vc, do = synth.make_csbp_rank(w, device=DEV)
+    qr, krs = csbp_ranges(w)
+    p = bd.make_problem(1, w.L, w.block_size, w.heads, w.kv_heads, w.head_dim, torch.bfloat16, out_f32=True)
+    n = w.local_tokens
+    ks = [kl.data_ptr()] + shard_views(kc, w)
+    vs = [vl.data_ptr()] + shard_views(vc, w)
+    o_parts, l_parts = [], []
+    for j, kr in enumerate(krs):
+        o = torch.empty(q.shape, dtype=F32, device=DEV)
+        lse = torch.empty((1, w.heads, n), dtype=F32, device=DEV)
+        bd.attn_partial_fwd(p, qr, q, o, lse, kr, ks[j], vs[j])
+        o_parts.append(o)
+        l_parts.append(lse)
+    om = torch.empty(q.shape, dtype=F32, device=DEV)
+    lm = torch.empty((1, w.heads, n), dtype=F32, device=DEV)
+    bd.lse_merge(o_parts, l_parts, om, lm)
+    of = torch.empty(q.shape, dtype=F32, device=DEV)
+    lf = torch.empty((1, w.heads, n), dtype=F32, device=DEV)
+    bd.attn_fwd(p, [qr], [q], [of], [lf], krs, ks, vs)
+    torch.cuda.synchronize()
+    for j in range(9, 17):  # shards 8..15 start at or after the first local block's position
+        if krs[j].pos0 >= w.local_pos0 + w.local_tokens - w.block_size:
+            assert torch.isneginf(l_parts[j]).all() and (o_parts[j] == 0).all()
+    # fused multi-range launch = merge of per-range partials (eq:correctness-online-softmax-merge)
+    assert_close("csbp fused vs merged O", of, om.cpu().double().numpy(), BF16)
+    assert_close("csbp fused vs merged LSE", lf, lm.cpu().double().numpy(), BF16)
+
+    dq = torch.empty(q.shape, dtype=F32, device=DEV)
+    dkl, dvl = (torch.empty(t.shape, dtype=F32, device=DEV) for t in (kl, vl))
+    dkc, dvc = (torch.empty(t.shape, dtype=F32, device=DEV) for t in (kc, vc))
+    ws = torch.empty(bd.attn_bwd_workspace_bytes(p, [qr]), dtype=torch.uint8, device=DEV)
+    bd.attn_bwd(p, [qr], [q], [om], [lm], [do], [dq], krs, ks, vs,
+                [dkl.data_ptr()] + shard_views(dkc, w), [dvl.data_ptr()] + shard_views(dvc, w), ws)
+    torch.cuda.synchronize()
+    dv_all = torch.cat([dvl, dvc], dim=1)
+    dv_identity(dv_all, do, w.heads // w.kv_heads, "csbp256k")
+    # shards whose positions no local block reaches get exact zeros
+    visible_end = w.local_pos0 + w.local_tokens - w.block_size
+    first_dead = -(-visible_end // w.shard_tokens)
+    assert (dkc[:, first_dead * w.shard_tokens:] == 0).all() and (dvc[:, first_dead * w.shard_tokens:] == 0).all()
+
+    kvs = [0, w.kv_heads - 1]
+    hs = kv_group_heads(w.heads, w.kv_heads, kvs)
+    qcpu, docpu = q[:, :, hs].cpu(), do[:, :, hs].cpu()
+    kall = torch.cat([kl, kc], dim=1)[:, :, kvs].cpu()
+    vall = torch.cat([vl, vc], dim=1)[:, :, kvs].cpu()
+    qranges = [(CORRUPTED, w.local_pos0, n)]
+    kranges = [(r.stream, r.pos0, r.len) for r in krs]
+    rng = np.random.default_rng(4)
+    rows = sorted(set([0, 31, 32, n // 2, n - 32, n - 1] + rng.choice(n, 16, replace=False).tolist()))
+    O, LSE = oracle.fwd(qcpu, kall, vall, qranges, kranges, w.block_size, q_rows=rows)
+    assert_close("csbp256k merged O rows", om[:, rows][:, :, hs], O, BF16)
+    assert_close("csbp256k merged LSE rows", lm[:, hs][:, :, rows], LSE, BF16)
+    single = [(CORRUPTED, w.local_pos0 + i, 1) for i in rows]
+    dQ, _, _ = oracle.bwd(qcpu[:, rows], kall, vall, O, LSE, docpu[:, rows], single, kranges, w.block_size)
+    assert_close("csbp256k dQ rows", dq[:, rows][:, :, hs], dQ, BF16)
+    # local corrupted blocks (block-local keys) and the tail of the partly visible shard
+    M = w.block_size
+    for blk in (0, n // M // 2, n // M - 1):
+        qrows = list(range(blk * M, (blk + 1) * M))
+        Oq, Lq = oracle.fwd(qcpu, kall, vall, qranges, kranges, M, q_rows=qrows)
+        single = [(CORRUPTED, w.local_pos0 + i, 1) for i in qrows]
+        _, dK, dV = oracle.bwd(qcpu[:, qrows], kall, vall, Oq, Lq, docpu[:, qrows], single, kranges, M)
+        kr = list(range(blk * M, (blk + 1) * M))
+        assert_close(f"csbp256k dK local block {blk}", dkl[:, kr][:, :, kvs], dK[:, kr], BF16)
+        assert_close(f"csbp256k dV local block {blk}", dvl[:, kr][:, :, kvs], dV[:, kr], BF16)
+    # clean keys of the last visible clean block: seen only by the last local block's queries
+    qrows = list(range(n - M, n))
+    Oq, Lq = oracle.fwd(qcpu, kall, vall, qranges, kranges, M, q_rows=qrows)
+    single = [(CORRUPTED, w.local_pos0 + i, 1) for i in qrows]
+    _, dK, dV = oracle.bwd(qcpu[:, qrows], kall, vall, Oq, Lq, docpu[:, qrows], single, kranges, M)
+    kpos = list(range(visible_end - M, visible_end))  # clean positions
+    krow = [n + x for x in kpos]  # rows in the concatenated [local ; clean] key tensor
+    assert_close("csbp256k dK last visible clean block", dkc[:, kpos][:, :, kvs], dK[:, krow], BF16)
+    assert_close("csbp256k dV last visible clean block", dvc[:, kpos][:, :, kvs], dV[:, krow], BF16)
