@@ -37,26 +37,32 @@ sys.path.insert(0, ROOT)
 METRIC = "BDLM attn fwd+bwd useful TFLOP/s & MFMA util at 32K ctx, 1 MI355X"
 PEAK_BF16_TFLOPS = 256 * 4096 * 2.4e9 / 1e12  # 256 CUs x 2048 bf16 FMA/clk/CU x 2 x 2.4 GHz = 2516.6
 PEAK_HBM_GBS = 8000.0
-KERNEL_SOURCES = ["common.hpp", "device.hpp", "bwd_bf16.hip"]
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_bwd_bf16_32k.json")
+# Sources each timed kernel is built from (a recorded counter value is only
+# trusted while these are unchanged).
+KERNEL_SOURCES = {
+    "fwd_bf16": ["common.hpp", "device.hpp", "qtiles.hpp", "fwd_bf16.hip"],
+    "bwd_dkdv_bf16": ["common.hpp", "device.hpp", "bwd_bf16.hip"],
+    "bwd_dq_bf16": ["common.hpp", "device.hpp", "qtiles.hpp", "bwd_dq.hip"],
+}
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_32k.json")
 
 
-def kernel_source_hash():
+def kernel_source_hash(kernel):
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in KERNEL_SOURCES.get(kernel, []):
         with open(os.path.join(ROOT, "paper_2609_19242_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
-def recorded_traffic():
-    """HBM bytes per launch of the fused backward from rocprofv3 PMC runs, if taken on this kernel source."""
+def recorded_traffic(kernel):
+    """HBM bytes per launch of `kernel` from rocprofv3 FETCH_SIZE/WRITE_SIZE runs, if taken on its current source."""
     try:
         with open(TRAFFIC_FILE) as f:
-            rec = json.load(f)
+            rec = json.load(f).get(kernel)
     except (OSError, ValueError):
         return None
-    if rec.get("kernel_source_sha256_16") != kernel_source_hash():
+    if not rec or rec.get("source_sha256_16") != kernel_source_hash(kernel):
         return None
     return rec.get("hbm_bytes_per_launch")
 
@@ -105,16 +111,20 @@ def bench_32k(torch, bd, synth, steps, warmup):
     kern = per_kernel(bd.timing_collect())
     ms = e0.elapsed_time(e1) / steps
     assert torch.isfinite(o).all() and torch.isfinite(dq).all()
+    # Algorithmic FLOP per valid pair of each kernel: forward 4d (Q K^T, P V);
+    # dK/dV kernel 8d (Q K^T, dO V^T, P^T dO, dS^T Q); dQ kernel 6d (Q K^T and
+    # dO V^T recomputed, dS K).  The useful total of a step stays 14d per pair.
+    per_pair = {"fwd_bf16": 4, "bwd_dkdv_bf16": 8, "bwd_dq_bf16": 6}
+    n_pairs = pairs * Hq * B
     for name, kd in kern.items():
-        if name == "fwd_bf16":
-            kd["useful_tflops"] = fl["fwd"] / (kd["avg_ms"] * 1e-3) / 1e12
-        elif name == "bwd_bf16":
-            kd["useful_tflops"] = fl["bwd"] / (kd["avg_ms"] * 1e-3) / 1e12
-    bwd_ms = kern["bwd_bf16"]["avg_ms"]
-    achieved = fl["bwd"] / (bwd_ms * 1e-3) / 1e12
-    roof = {"bound": "mfma", "kernel": "bwd_bf16", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
-            "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": recorded_traffic(),
-            "flop_per_launch": fl["bwd"], "avg_launch_ms": bwd_ms}
+        if name in per_pair:
+            kd["flop_per_launch"] = per_pair[name] * D * n_pairs
+            kd["tflops"] = kd["flop_per_launch"] / (kd["avg_ms"] * 1e-3) / 1e12
+    dom = max(kern, key=lambda n: kern[n]["avg_ms"])
+    achieved = kern[dom]["tflops"]
+    roof = {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": recorded_traffic(dom),
+            "flop_per_launch": kern[dom]["flop_per_launch"], "avg_launch_ms": kern[dom]["avg_ms"]}
     res = {"ms_per_step": ms, "wall_s": wall, "pairs_per_head": pairs, "flops": fl, "kernels": kern,
            "roofline": roof, "value": fl["total"] / (ms * 1e-3) / 1e12, "workload": w}
     del q, k, v, do, o, lse, dq, dk, dv, ws

@@ -89,6 +89,11 @@ typedef struct {
   float scale;        /* softmax scale; <= 0 selects 1 / sqrt(head_dim) */
   int32_t clean_intra;/* bdlm_clean_intra */
   int32_t out_f32;    /* 0: O, dQ, dK, dV in `dtype`; 1: in fp32 (the fp32 accumulators, unrounded) */
+  int32_t hilo;       /* bf16 path: 0 rounds the softmax probabilities P and dS = P (dP - D) to
+                         bf16 for the P V, P^T dO, dS K and dS^T Q products; 1 carries each as a
+                         two-term bf16 sum hi + lo (about 16 significant bits, up to 1.5x the
+                         matrix work of those products), for inputs with large scores or |dS|,
+                         e.g. keys of large norm.  Ignored by the fp32 path. */
 } bdlm_problem;
 
 /* A run of rows of one stream (see "Rows and ranges" above). */
@@ -149,8 +154,8 @@ bdlm_status bdlm_lse_merge(int64_t batch, int64_t rows, int32_t heads, int32_t h
                            const float* const* lse_parts, int32_t part_dtype,
                            void* o, float* lse, int32_t out_dtype, hipStream_t stream);
 
-/* Workspace bytes bdlm_attn_bwd needs for these query ranges (fp32 dQ
- * accumulator and the row dots D = rowsum(dO * O)). */
+/* Workspace bytes bdlm_attn_bwd needs for these query ranges: the fp32 row
+ * dots D = rowsum(dO * O), batch * len * heads floats per range. */
 size_t bdlm_attn_bwd_workspace_bytes(const bdlm_problem* p, int32_t n_q, const bdlm_range* q_ranges);
 
 /*

@@ -33,7 +33,9 @@ CLEAN_INTRA_CAUSAL, CLEAN_INTRA_BLOCK = 0, 1
 MAX_Q_RANGES, MAX_K_RANGES, MAX_MERGE_PARTS = 4, 32, 32
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-library_path = os.path.join(_HERE, "libbdlm_attn.so")
+# BDLM_LIBRARY points the binding at another build of the same C ABI (e.g. a
+# differently tuned one); the default is the in-tree library.
+library_path = os.environ.get("BDLM_LIBRARY") or os.path.join(_HERE, "libbdlm_attn.so")
 
 
 class Problem(ctypes.Structure):
@@ -41,7 +43,7 @@ class Problem(ctypes.Structure):
         ("batch", ctypes.c_int64), ("L", ctypes.c_int64), ("block_size", ctypes.c_int64),
         ("heads", ctypes.c_int32), ("kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
         ("dtype", ctypes.c_int32), ("scale", ctypes.c_float), ("clean_intra", ctypes.c_int32),
-        ("out_f32", ctypes.c_int32),
+        ("out_f32", ctypes.c_int32), ("hilo", ctypes.c_int32),
     ]
 
 
@@ -147,9 +149,11 @@ def _dtype_code(dt: torch.dtype) -> int:
 
 
 def make_problem(batch: int, L: int, block_size: int, heads: int, kv_heads: int, head_dim: int,
-                 dtype, scale: float = 0.0, clean_intra: int = CLEAN_INTRA_CAUSAL, out_f32: bool = False) -> Problem:
+                 dtype, scale: float = 0.0, clean_intra: int = CLEAN_INTRA_CAUSAL, out_f32: bool = False,
+                 hilo: bool = False) -> Problem:
     code = dtype if isinstance(dtype, int) else _dtype_code(dtype)
-    return Problem(batch, L, block_size, heads, kv_heads, head_dim, code, scale, clean_intra, int(bool(out_f32)))
+    return Problem(batch, L, block_size, heads, kv_heads, head_dim, code, scale, clean_intra, int(bool(out_f32)),
+                   int(bool(hilo)))
 
 
 def joint_ranges(L: int) -> List[Range]:
@@ -229,7 +233,7 @@ def _check_joint(q, k, v):
 
 
 def joint_fwd(q, k, v, block_size: int, clean_intra: int = CLEAN_INTRA_CAUSAL, scale: float = 0.0,
-              out_f32: bool = False, out: Optional[tuple] = None, stream=None):
+              out_f32: bool = False, out: Optional[tuple] = None, stream=None, hilo: bool = False):
     """Fused forward over packed ``[x_t ; x]`` tensors ``q [B][2L][Hq][D]``, ``k, v [B][2L][Hkv][D]``.
 
     Returns ``(o, lse)`` with ``lse [B][Hq][2L]`` fp32; ``o`` is fp32 when ``out_f32``.
@@ -237,7 +241,7 @@ def joint_fwd(q, k, v, block_size: int, clean_intra: int = CLEAN_INTRA_CAUSAL, s
     _check_joint(q, k, v)
     B, n, Hq, D = q.shape
     L = n // 2
-    p = make_problem(B, L, block_size, Hq, k.shape[2], D, q.dtype, scale, clean_intra, out_f32)
+    p = make_problem(B, L, block_size, Hq, k.shape[2], D, q.dtype, scale, clean_intra, out_f32, hilo)
     odt = torch.float32 if out_f32 else q.dtype
     o, lse = out if out is not None else (torch.empty(q.shape, dtype=odt, device=q.device),
                                           torch.empty((B, Hq, n), dtype=torch.float32, device=q.device))
@@ -249,12 +253,12 @@ def joint_fwd(q, k, v, block_size: int, clean_intra: int = CLEAN_INTRA_CAUSAL, s
 
 def joint_bwd(q, k, v, o, lse, do, block_size: int, clean_intra: int = CLEAN_INTRA_CAUSAL, scale: float = 0.0,
               out_f32: bool = False, out: Optional[tuple] = None, workspace: Optional[torch.Tensor] = None,
-              stream=None):
+              stream=None, hilo: bool = False):
     """Backward of :func:`joint_fwd`; returns ``(dq, dk, dv)`` (fp32 when ``out_f32``; ``o`` must match)."""
     _check_joint(q, k, v)
     B, n, Hq, D = q.shape
     L = n // 2
-    p = make_problem(B, L, block_size, Hq, k.shape[2], D, q.dtype, scale, clean_intra, out_f32)
+    p = make_problem(B, L, block_size, Hq, k.shape[2], D, q.dtype, scale, clean_intra, out_f32, hilo)
     r = joint_ranges(L)
     odt = torch.float32 if out_f32 else q.dtype
     if o.dtype != odt:

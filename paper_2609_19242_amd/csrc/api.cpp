@@ -1,6 +1,6 @@
 // C ABI of the BDLM attention library: argument validation, kernel argument
 // construction and launches.  Declarations and contracts: include/bdlm_attn.h.
-#include "../../include/bdlm_attn.h"
+#include "bdlm_attn.h"
 
 #include <hip/hip_runtime.h>
 
@@ -33,9 +33,9 @@ bdlm_status hip_fail(hipError_t e, const char* what) {
 }
 
 // ---- per-thread kernel timing (bdlm_timing_enable / bdlm_timing_collect)
-enum KernelId { kKFwdBf16 = 0, kKFwdF32, kKMerge, kKBwdPre, kKBwdBf16, kKBwdPost, kKBwdF32, kKCount };
-const char* const kKernelNames[kKCount] = {"fwd_bf16", "fwd_f32", "lse_merge", "bwd_pre", "bwd_bf16", "bwd_post",
-                                           "bwd_f32"};
+enum KernelId { kKFwdBf16 = 0, kKFwdF32, kKMerge, kKBwdPre, kKBwdBf16, kKBwdDq, kKBwdF32, kKCount };
+const char* const kKernelNames[kKCount] = {"fwd_bf16", "fwd_f32", "lse_merge", "bwd_pre", "bwd_dkdv_bf16",
+                                           "bwd_dq_bf16", "bwd_f32"};
 struct TimingRec {
   int id;
   hipEvent_t a, b;
@@ -92,6 +92,7 @@ bdlm_status check_problem(const bdlm_problem* p) {
     return fail(BDLM_ERR_INVALID, "clean_intra %d is not a bdlm_clean_intra value", p->clean_intra);
   if (!std::isfinite(p->scale)) return fail(BDLM_ERR_INVALID, "scale is not finite");
   if (p->out_f32 != 0 && p->out_f32 != 1) return fail(BDLM_ERR_INVALID, "out_f32 must be 0 or 1");
+  if (p->hilo != 0 && p->hilo != 1) return fail(BDLM_ERR_INVALID, "hilo must be 0 or 1");
   return BDLM_OK;
 }
 
@@ -131,6 +132,7 @@ void fill_common(AttnArgs& a, const bdlm_problem* p) {
   a.scale = resolved_scale(p);
   a.scale_log2 = a.scale * 1.44269504088896340736f;
   a.out_f32 = (p->dtype == BDLM_F32 || p->out_f32) ? 1 : 0;
+  a.hilo = p->hilo;
 }
 
 void fill_q(QRangeArg& d, const bdlm_range& r) {
@@ -283,8 +285,7 @@ size_t bdlm_attn_bwd_workspace_bytes(const bdlm_problem* p, int32_t n_q, const b
   size_t tot = 0;
   for (int i = 0; i < n_q; ++i) {
     const size_t rows = (size_t)p->batch * (size_t)(q_ranges[i].len > 0 ? q_ranges[i].len : 0);
-    tot += align256(rows * p->heads * p->head_dim * sizeof(float));  // dQ accumulator
-    tot += align256(rows * p->heads * sizeof(float));                // D = rowsum(dO * O)
+    tot += align256(rows * p->heads * sizeof(float));  // D = rowsum(dO * O)
   }
   return tot;
 }
@@ -325,8 +326,6 @@ bdlm_status bdlm_attn_bwd(const bdlm_problem* p, int32_t n_q, const bdlm_range* 
     a.qr[i].dO = dO[i];
     a.qr[i].dq = dq[i];
     const size_t rows = (size_t)p->batch * (size_t)r.len;
-    a.qr[i].dqacc = reinterpret_cast<float*>(ws);
-    ws += align256(rows * p->heads * p->head_dim * sizeof(float));
     a.qr[i].delta = reinterpret_cast<float*>(ws);
     ws += align256(rows * p->heads * sizeof(float));
   }
@@ -367,9 +366,17 @@ bdlm_status bdlm_attn_bwd(const bdlm_problem* p, int32_t n_q, const bdlm_range* 
   if (e != hipSuccess) return hip_fail(e, "backward pre-pass launch");
   if (p->dtype == BDLM_BF16) {
     e = timed(kKBwdBf16, stream, [&] { return launch_bwd_bf16(a, p->head_dim, stream); });
-    if (e != hipSuccess) return hip_fail(e, "backward launch");
-    e = timed(kKBwdPost, stream, [&] { return launch_bwd_post_bf16(a, p->head_dim, stream); });
-    if (e != hipSuccess) return hip_fail(e, "backward post-pass launch");
+    if (e != hipSuccess) return hip_fail(e, "backward dK/dV launch");
+    // The dQ kernel walks query tiles of the forward's height.
+    AttnArgs aq = a;
+    const int64_t qt = tile_ranges(aq.qr, n_q, kFwdRowsBf16);
+    if ((st = check_grid(qt, (int64_t)p->heads * p->batch)) != BDLM_OK) return st;
+    aq.total_tiles = (int32_t)qt;
+    aq.interleave = 1;
+    for (int i = 1; i < n_q; ++i)
+      if (aq.qr[i].ntiles != aq.qr[0].ntiles) aq.interleave = 0;
+    e = timed(kKBwdDq, stream, [&] { return launch_bwd_dq_bf16(aq, p->head_dim, stream); });
+    if (e != hipSuccess) return hip_fail(e, "backward dQ launch");
   } else {
     e = timed(kKBwdF32, stream, [&] { return launch_bwd_f32(a, p->head_dim, stream); });
     if (e != hipSuccess) return hip_fail(e, "backward launch");

@@ -1,25 +1,23 @@
-// Fused mask-aware BDLM attention backward, bf16 inputs, fp32 accumulation, gfx950.
+// dK and dV of the BDLM attention backward, key-major, bf16 inputs, fp32 accumulation, gfx950.
 //
 // Exact gradients from the saved O and LSE (arXiv 2609.19242 App. C fused
-// backward; eqs. eq:correctness-corrupted-gradient to
-// eq:correctness-query-gradient): with P = exp(scale Q K^T + mask - LSE) and
-// D = rowsum(dO * O) (from the pre pass),
-//   dV = P^T dO,  dS = P * (dO V^T - D),  dK = scale dS^T Q,  dQ = scale dS K,
-// where dK/dV sum over every query row of every query range and over the query
-// heads of the KV head's GQA group.
+// backward; eq:correctness-corrupted-gradient and eq:correctness-clean-gradient):
+// with P = exp(scale Q K^T + mask - LSE) and D = rowsum(dO * O) (pre pass),
+//   dV = P^T dO,  dS = P * (dO V^T - D),  dK = scale dS^T Q,
+// summed over every query row of every query range and over the query heads
+// of the KV head's GQA group.  dQ comes from the query-major kernel in
+// bwd_dq.hip, so this kernel needs no atomics.
 //
-// KV-major: a workgroup owns 128 keys of one KV head (4 waves x 32 keys), holds
-// their K and V rows in registers as MFMA operands and accumulates dK^T and
-// dV^T in registers for the whole pass.  It walks the query heads of the group
-// and, for each query range, the 32-row query steps that can see its keys (the
+// A workgroup owns 128 keys of one KV head (4 waves x 32 keys), holds their K
+// and V rows in registers as MFMA operands and accumulates dK^T and dV^T in
+// registers for the whole pass.  It walks the query heads of the group and,
+// for each query range, the 32-row query steps that can see its keys (the
 // query-side intervals of common.hpp give the span in closed form; steps every
 // key sees completely skip the mask test).  Per step and wave:
-//   S = Q K^T, dP = dO V^T      (Q, dO rows from LDS as A, K, V from registers as B)
+//   S = Q K^T, dP = dO V^T          (Q, dO rows from LDS as A, K, V from registers as B)
 //   dV^T += dO^T P, dK^T += Q^T dS  (dO^T, Q^T via LDS transpose reads; P, dS from registers)
-//   dQ[:, slice] += dS K        (dS^T staged in LDS, K tile in LDS, both via transpose reads)
-// dQ partial sums go to an fp32 accumulator with global atomics; a post pass
-// scales and rounds it.  Q/dO/LSE/D of the next step are prefetched into
-// registers while the current step computes.
+// Q/dO/LSE/D of the next step are prefetched into registers at the top of the
+// step and stored to the other LDS stage in its middle; one barrier per step.
 #include "common.hpp"
 #include "device.hpp"
 
@@ -29,20 +27,14 @@ namespace {
 
 constexpr float kLog2e = 1.44269504088896340736f;
 
-template <int D>
+template <int D, bool HILO>
 __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
   constexpr int BN = kBwdKeysBf16, BM = 32, PITCH = D + 16, KS = D / 16, DT = D / 32, NT = 256;
-  constexpr int DSP = 48;  // dS^T row pitch: 32 queries + pad
   constexpr int CPR = D / 8;
   constexpr int QCPT = BM * CPR / NT;
   static_assert(BN == 128 && (BM * CPR) % NT == 0, "tile shape");
-  constexpr int NSL = D / 32;           // dQ column slices of 32
-  constexpr int NPART = 4 / NSL;        // waves per slice (split over keys)
-  constexpr int QKSTEPS = (BN / 16) / NPART;
-  __shared__ __attribute__((aligned(16))) bf16 k_lds[BN * PITCH];
   __shared__ __attribute__((aligned(16))) bf16 q_lds[2][BM * PITCH];
   __shared__ __attribute__((aligned(16))) bf16 do_lds[2][BM * PITCH];
-  __shared__ __attribute__((aligned(16))) bf16 ds_lds[BN * DSP];
   __shared__ __attribute__((aligned(16))) float st_lds[2][2][BM];  // [stage][lse*log2e | D][row]
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -76,7 +68,7 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
   const int pk = kr.pos0 + key0 + imin(mykey, nk - 1);
   const int kpos_first = kr.pos0 + key0, kpos_last = kr.pos0 + key0 + nk - 1;
 
-  // ---- K, V rows of this wave's keys (B operands) and the K tile in LDS
+  // ---- K, V rows of this wave's keys (B operands)
   bf16x8 kf[KS], vf[KS];
   {
     const int64_t eoff = (((int64_t)b * kr.bstride + key0) * HKV + kvh) * D;
@@ -88,7 +80,6 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
     for (int s = 0; s < KS; ++s) {
       kf[s] = __builtin_bit_cast(bf16x8, buf_load16(rk, off + 32 * s));
       vf[s] = __builtin_bit_cast(bf16x8, buf_load16(rv, off + 32 * s));
-      *(bf16x8*)(k_lds + mykey * PITCH + 16 * s + 8 * half) = kf[s];
     }
   }
 
@@ -130,7 +121,8 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
   };
 
   u32x4 pq[QCPT], pdo[QCPT];
-  float pst = 0.f;
+  float pz = 0.f, pd = 0.f;  // raw LSE and D of row (tid % 32) of the prefetched step
+  int prow_ok = 0;
   auto load_step = [&](int slot, int step) {
     const QRangeArg& qr = a.qr[slot % a.n_q];
     const int h = kvh * a.group + slot / a.n_q;
@@ -148,15 +140,13 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
       pq[n] = buf_load16(rq, off);
       pdo[n] = buf_load16(rdo, off);
     }
-    if (tid < 2 * BM) {
-      const int row = row0 + (tid & (BM - 1));
-      if (tid < BM) {
-        const float z = row < qr.len ? qr.lse[((int64_t)b * H + h) * qr.bstride + row] : -INFINITY;
-        pst = (z == -INFINITY) ? INFINITY : z * kLog2e;  // rows seeing nothing get P = 0
-      } else {
-        pst = row < qr.len ? qr.delta[((int64_t)b * H + h) * qr.len + row] : 0.f;
-      }
-    }
+    // Branch-free: every lane reads row (tid % 32)'s LSE and D; the values
+    // are only interpreted when stored, so nothing waits on them here.
+    const auto rl = make_rsrc(qr.lse + ((int64_t)b * H + h) * qr.bstride + row0, (uint32_t)nrows * 4);
+    const auto rd = make_rsrc(qr.delta + ((int64_t)b * H + h) * qr.len + row0, (uint32_t)nrows * 4);
+    pz = buf_load_f32(rl, (uint32_t)(tid & (BM - 1)) * 4);
+    pd = buf_load_f32(rd, (uint32_t)(tid & (BM - 1)) * 4);
+    prow_ok = (tid & (BM - 1)) < nrows;
   };
   auto store_step = [&](int stage) {
 #pragma unroll
@@ -166,7 +156,9 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
       *(u32x4*)(&q_lds[stage][row * PITCH + col * 8]) = pq[n];
       *(u32x4*)(&do_lds[stage][row * PITCH + col * 8]) = pdo[n];
     }
-    if (tid < 2 * BM) st_lds[stage][tid / BM][tid & (BM - 1)] = pst;
+    // Rows past the range end and rows that see no key get LSE = +inf (P = 0) and D = 0.
+    if (tid < BM) st_lds[stage][0][tid] = (prow_ok && pz != -INFINITY) ? pz * kLog2e : INFINITY;
+    else if (tid < 2 * BM) st_lds[stage][1][tid - BM] = prow_ok ? pd : 0.f;
   };
 
   int slot = 0, s = 0, s1 = 0, f0 = 0, f1 = 0;
@@ -177,13 +169,19 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
   }
   __syncthreads();
 
+  // One barrier per step: Q/dO/LSE/D of step n+1 are stored to the other
+  // stage during step n; that stage was last read before the previous barrier.
   int cur = 0, lane_range = -1, lane_qa = 0, lane_qw = 0;
   const float c = a.scale_log2;
   while (have) {
     int slotn = slot, sn = s + 1, s1n = s1, f0n = f0, f1n = f1;
     bool have_next = sn < s1;
     if (!have_next) have_next = find_from(slot + 1, slotn, sn, s1n, f0n, f1n);
+    // Unconditional prefetch (the last step re-reads its own rows) keeps the
+    // loads at the top of the step, a full step ahead of their LDS store.
     if (have_next) load_step(slotn, sn);
+    else load_step(slot, s);
+    __builtin_amdgcn_sched_barrier(0);
 
     const int qi = slot % a.n_q;
     const QRangeArg& qr = a.qr[qi];
@@ -198,89 +196,82 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
       lane_range = qi;
     }
 
-    // S = Q K^T and dP = dO V^T for this wave's 32 keys.
+    // S = Q K^T and dP = dO V^T for this wave's 32 keys (A operands read up front).
+    const bf16* qs = &q_lds[cur][0];
+    const bf16* dos = &do_lds[cur][0];
     f32x16 sacc, dpacc;
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      sacc[i] = 0.f;
-      dpacc[i] = 0.f;
-    }
     {
-      const bf16* qa = &q_lds[cur][l32 * PITCH + 8 * half];
-      const bf16* da = &do_lds[cur][l32 * PITCH + 8 * half];
+      bf16x8 qa[KS], da[KS];
 #pragma unroll
       for (int k = 0; k < KS; ++k) {
-        sacc = mfma32(*(const bf16x8*)(qa + 16 * k), kf[k], sacc);
-        dpacc = mfma32(*(const bf16x8*)(da + 16 * k), vf[k], dpacc);
+        qa[k] = *(const bf16x8*)(qs + l32 * PITCH + 8 * half + 16 * k);
+        da[k] = *(const bf16x8*)(dos + l32 * PITCH + 8 * half + 16 * k);
       }
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        sacc[i] = 0.f;
+        dpacc[i] = 0.f;
+      }
+#pragma unroll
+      for (int k = 0; k < KS; ++k) {
+        sacc = mfma32(qa[k], kf[k], sacc);
+        dpacc = mfma32(da[k], vf[k], dpacc);
+      }
+    }
+    // dO^T and Q^T fragments for dV and dK, and the rows' LSE and D.
+    bf16x8 doT[2][DT], qT[2][DT];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int off = (16 * u + 4 * (G >> 1) + (sl >> 2)) * PITCH + 16 * (G & 1) + 4 * (sl & 3);
+#pragma unroll
+      for (int d = 0; d < DT; ++d) {
+        doT[u][d] = cat(lds_read_tr(dos + off + 32 * d), lds_read_tr(dos + off + 32 * d + 8 * PITCH));
+        qT[u][d] = cat(lds_read_tr(qs + off + 32 * d), lds_read_tr(qs + off + 32 * d + 8 * PITCH));
+      }
+    }
+    f32x4 l2[4], dl[4];
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4) {
+      l2[g4] = *(const f32x4*)(&st_lds[cur][0][8 * g4 + 4 * half]);
+      dl[g4] = *(const f32x4*)(&st_lds[cur][1][8 * g4 + 4 * half]);
     }
 
     // P = exp2(S c - LSE log2 e), dS = P (dP - D); the mask only where needed.
-    const bool need_mask = !(s >= f0 && s < f1);
-    const int mbase = qr.pos0 + s * BM + 4 * half - lane_qa;
-    bf16x8 pb[2], dsb[2];
-    bf16x4 dst[4];
+    if (!(s >= f0 && s < f1)) {  // partly visible step: hide the masked pairs (P = 0)
+      const int mbase = qr.pos0 + s * BM + 4 * half - lane_qa;
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        if ((unsigned)(mbase + 8 * (i >> 2) + (i & 3)) >= (unsigned)lane_qw) sacc[i] = -INFINITY;
+    }
+    bf16x8 pb[2], pl[2], dsb[2], dsl[2];
 #pragma unroll
     for (int g4 = 0; g4 < 4; ++g4) {
-      const f32x4 l2 = *(const f32x4*)(&st_lds[cur][0][8 * g4 + 4 * half]);
-      const f32x4 dl = *(const f32x4*)(&st_lds[cur][1][8 * g4 + 4 * half]);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int i = 4 * g4 + e;
-        float p = exp2f_fast(fmaf(sacc[i], c, -l2[e]));
-        if (need_mask && (unsigned)(mbase + 8 * g4 + e) >= (unsigned)lane_qw) p = 0.f;
-        const float ds = p * (dpacc[i] - dl[e]);
-        pb[i >> 3][i & 7] = to_bf16(p);
-        const bf16 dsh = to_bf16(ds);
-        dsb[i >> 3][i & 7] = dsh;
-        dst[g4][e] = dsh;
+        const float p = exp2f_fast(fmaf(sacc[i], c, -l2[g4][e]));
+        const float ds = p * (dpacc[i] - dl[g4][e]);
+        const bf16 phi = to_bf16(p);
+        pb[i >> 3][i & 7] = phi;
+        if constexpr (HILO) pl[i >> 3][i & 7] = to_bf16(p - (float)phi);
+        const bf16 hi = to_bf16(ds);
+        dsb[i >> 3][i & 7] = hi;
+        if constexpr (HILO) dsl[i >> 3][i & 7] = to_bf16(ds - (float)hi);
       }
     }
+    store_step(cur ^ 1);
 
     // dV^T += dO^T P and dK^T += Q^T dS (queries are the contraction index).
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int qrow = 16 * u + 4 * (G >> 1) + (sl >> 2);
-      const bf16* dop = &do_lds[cur][qrow * PITCH + 16 * (G & 1) + 4 * (sl & 3)];
-      const bf16* qp = &q_lds[cur][qrow * PITCH + 16 * (G & 1) + 4 * (sl & 3)];
+    for (int u = 0; u < 2; ++u)
 #pragma unroll
       for (int d = 0; d < DT; ++d) {
-        const bf16x8 av = cat(lds_read_tr(dop + 32 * d), lds_read_tr(dop + 32 * d + 8 * PITCH));
-        dva[d] = mfma32(av, pb[u], dva[d]);
-        const bf16x8 aq = cat(lds_read_tr(qp + 32 * d), lds_read_tr(qp + 32 * d + 8 * PITCH));
-        dka[d] = mfma32(aq, dsb[u], dka[d]);
+        dva[d] = mfma32(doT[u][d], pb[u], dva[d]);
+        if constexpr (HILO) dva[d] = mfma32(doT[u][d], pl[u], dva[d]);
+        dka[d] = mfma32(qT[u][d], dsb[u], dka[d]);
+        if constexpr (HILO) dka[d] = mfma32(qT[u][d], dsl[u], dka[d]);
       }
-    }
 
-    // dS^T to LDS for the dQ product.
-#pragma unroll
-    for (int g4 = 0; g4 < 4; ++g4) *(bf16x4*)(ds_lds + mykey * DSP + 8 * g4 + 4 * half) = dst[g4];
-    __syncthreads();
-
-    {
-      const int slice = w % NSL, part = w / NSL;
-      f32x16 dqa;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) dqa[i] = 0.f;
-#pragma unroll
-      for (int kk = 0; kk < QKSTEPS; ++kk) {
-        const int krow = 16 * (part * QKSTEPS + kk) + 8 * (G >> 1) + (sl >> 2);
-        const bf16* ap = ds_lds + krow * DSP + 16 * (G & 1) + 4 * (sl & 3);
-        const bf16* bp = k_lds + krow * PITCH + 32 * slice + 16 * (G & 1) + 4 * (sl & 3);
-        const bf16x8 av = cat(lds_read_tr(ap), lds_read_tr(ap + 4 * DSP));
-        const bf16x8 bv = cat(lds_read_tr(bp), lds_read_tr(bp + 4 * PITCH));
-        dqa = mfma32(av, bv, dqa);
-      }
-      const int row0 = s * BM;
-      float* accp = qr.dqacc + (((int64_t)b * qr.len + row0) * H + h) * D + 32 * slice + l32;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int q = 8 * (i >> 2) + 4 * half + (i & 3);
-        if (row0 + q < qr.len) unsafeAtomicAdd(accp + (int64_t)q * H * D, dqa[i]);
-      }
-    }
-
-    if (have_next) store_step(cur ^ 1);
     __syncthreads();
     cur ^= 1;
     slot = slotn; s = sn; s1 = s1n; f0 = f0n; f1 = f1n;
@@ -331,10 +322,13 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
 hipError_t launch_bwd_bf16(const AttnArgs& a, int head_dim, hipStream_t s) {
   const int n = a.total_tiles * a.kv_heads * a.batch;
   if (n == 0) return hipSuccess;
-  if (head_dim == 128)
-    hipLaunchKernelGGL((bwd_bf16_kernel<128>), dim3(n), dim3(256), 0, s, a);
-  else
-    hipLaunchKernelGGL((bwd_bf16_kernel<64>), dim3(n), dim3(256), 0, s, a);
+  if (head_dim == 128) {
+    if (a.hilo) hipLaunchKernelGGL((bwd_bf16_kernel<128, true>), dim3(n), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((bwd_bf16_kernel<128, false>), dim3(n), dim3(256), 0, s, a);
+  } else {
+    if (a.hilo) hipLaunchKernelGGL((bwd_bf16_kernel<64, true>), dim3(n), dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((bwd_bf16_kernel<64, false>), dim3(n), dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 

@@ -1,9 +1,7 @@
-// Backward pre- and post-processing, gfx950 (HBM-bound elementwise passes).
+// Backward pre-pass, gfx950 (an HBM-bound elementwise pass).
 //
-// pre:  D[b][h][row] = sum_d dO * O in fp32 (the row dot the softmax gradient
-//       dS = P * (dP - D) needs; arXiv 2609.19242 App. C reuses the saved O)
-//       and, for the bf16 path, zero the fp32 dQ accumulator.
-// post: dQ = bf16(scale * accumulator).
+// D[b][h][row] = sum_d dO * O in fp32: the row dot the softmax gradient
+// dS = P * (dP - D) needs (arXiv 2609.19242 App. C reuses the saved O).
 // One thread per 8 consecutive head_dim elements; the D/8 threads of one
 // (row, head) are adjacent lanes and reduce with cross-lane shuffles.
 #include "common.hpp"
@@ -14,7 +12,7 @@ namespace bdlm {
 namespace {
 
 template <int D, typename T, typename TO>
-__global__ __launch_bounds__(256) void bwd_pre_kernel(const AttnArgs a, int zero_acc) {
+__global__ __launch_bounds__(256) void bwd_pre_kernel(const AttnArgs a) {
   constexpr int CPR = D / 8;
   const QRangeArg& qr = a.qr[blockIdx.y];
   const int64_t H = a.heads;
@@ -54,41 +52,6 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(const AttnArgs a, int zero
   for (int w = CPR / 2; w > 0; w >>= 1) s += __shfl_xor(s, w, CPR);
   if (!ok) return;
   if (chunk == 0) qr.delta[(b * H + h) * qr.len + row] = s;
-  if (zero_acc) {
-    f32x4 z = {0.f, 0.f, 0.f, 0.f};
-    f32x4* p = (f32x4*)(qr.dqacc + rh * D + chunk * 8);
-    p[0] = z;
-    p[1] = z;
-  }
-}
-
-template <int D>
-__global__ __launch_bounds__(256) void bwd_post_kernel(const AttnArgs a) {
-  constexpr int CPR = D / 8;
-  const QRangeArg& qr = a.qr[blockIdx.y];
-  const int64_t H = a.heads;
-  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (gid >= (int64_t)a.batch * qr.len * H * CPR) return;
-  const int chunk = (int)(gid % CPR);
-  const int64_t rh = gid / CPR;
-  const int64_t h = rh % H, brow = rh / H;
-  const int64_t row = brow % qr.len, b = brow / qr.len;
-  const f32x4* src = (const f32x4*)(qr.dqacc + rh * D + chunk * 8);
-  const f32x4 x0 = src[0], x1 = src[1];
-  const int64_t dst = ((b * qr.bstride + row) * H + h) * D + chunk * 8;
-  if (a.out_f32) {
-    f32x4* y = (f32x4*)((float*)qr.dq + dst);
-    y[0] = x0 * a.scale;
-    y[1] = x1 * a.scale;
-  } else {
-    bf16x8 y;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      y[e] = to_bf16(x0[e] * a.scale);
-      y[4 + e] = to_bf16(x1[e] * a.scale);
-    }
-    *(bf16x8*)((bf16*)qr.dq + dst) = y;
-  }
 }
 
 int64_t max_q_threads(const AttnArgs& a, int cpr) {
@@ -106,26 +69,16 @@ hipError_t launch_bwd_pre(const AttnArgs& a, int head_dim, int dtype, hipStream_
   const int64_t t = max_q_threads(a, head_dim / 8);
   if (t == 0) return hipSuccess;
   const dim3 grid((unsigned)((t + 255) / 256), a.n_q);
-  const int zero = dtype == 0;
   if (dtype == 0 && !a.out_f32) {
-    if (head_dim == 128) hipLaunchKernelGGL((bwd_pre_kernel<128, bf16, bf16>), grid, dim3(256), 0, s, a, zero);
-    else hipLaunchKernelGGL((bwd_pre_kernel<64, bf16, bf16>), grid, dim3(256), 0, s, a, zero);
+    if (head_dim == 128) hipLaunchKernelGGL((bwd_pre_kernel<128, bf16, bf16>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((bwd_pre_kernel<64, bf16, bf16>), grid, dim3(256), 0, s, a);
   } else if (dtype == 0) {
-    if (head_dim == 128) hipLaunchKernelGGL((bwd_pre_kernel<128, bf16, float>), grid, dim3(256), 0, s, a, zero);
-    else hipLaunchKernelGGL((bwd_pre_kernel<64, bf16, float>), grid, dim3(256), 0, s, a, zero);
+    if (head_dim == 128) hipLaunchKernelGGL((bwd_pre_kernel<128, bf16, float>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((bwd_pre_kernel<64, bf16, float>), grid, dim3(256), 0, s, a);
   } else {
-    if (head_dim == 128) hipLaunchKernelGGL((bwd_pre_kernel<128, float, float>), grid, dim3(256), 0, s, a, zero);
-    else hipLaunchKernelGGL((bwd_pre_kernel<64, float, float>), grid, dim3(256), 0, s, a, zero);
+    if (head_dim == 128) hipLaunchKernelGGL((bwd_pre_kernel<128, float, float>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((bwd_pre_kernel<64, float, float>), grid, dim3(256), 0, s, a);
   }
-  return hipGetLastError();
-}
-
-hipError_t launch_bwd_post_bf16(const AttnArgs& a, int head_dim, hipStream_t s) {
-  const int64_t t = max_q_threads(a, head_dim / 8);
-  if (t == 0) return hipSuccess;
-  const dim3 grid((unsigned)((t + 255) / 256), a.n_q);
-  if (head_dim == 128) hipLaunchKernelGGL((bwd_post_kernel<128>), grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL((bwd_post_kernel<64>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -79,7 +79,6 @@ struct QRangeArg {
   float* lse;
   const void* dO;
   void* dq;
-  float* dqacc;       // fp32 dQ accumulator [batch][len][heads][d]
   float* delta;       // D = rowsum(dO * O), [batch][heads][len]
 };
 
@@ -106,6 +105,7 @@ struct AttnArgs {
   int32_t total_tiles;   // flattened tiles (query tiles for fwd, key tiles for bwd)
   int32_t interleave;    // fwd: query ranges have equal tile counts, visit them round-robin
   int32_t out_f32;       // O, dQ, dK, dV are fp32 (else the input dtype)
+  int32_t hilo;          // P and dS enter their products as bf16 hi + lo
   int32_t order[kMaxK];  // bwd: visiting order of key ranges (heaviest first)
   QRangeArg qr[kMaxQ];
   KRangeArg kr[kMaxK];
@@ -137,11 +137,11 @@ hipError_t launch_fwd_f32(const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_merge(const MergeArgs& a, int head_dim, int part_dtype, int out_dtype, hipStream_t s);
 hipError_t launch_bwd_pre(const AttnArgs& a, int head_dim, int dtype, hipStream_t s);
 hipError_t launch_bwd_bf16(const AttnArgs& a, int head_dim, hipStream_t s);
-hipError_t launch_bwd_post_bf16(const AttnArgs& a, int head_dim, hipStream_t s);
+hipError_t launch_bwd_dq_bf16(const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_bwd_f32(const AttnArgs& a, int head_dim, hipStream_t s);
 
 // Tile heights the launchers use (the C ABI fills ntiles/tile0 with them).
-constexpr int kFwdRowsBf16 = 256;  // query rows per forward workgroup (8 waves x 32)
+constexpr int kFwdRowsBf16 = 256;  // query rows per forward / dQ workgroup (8 waves x 32)
 constexpr int kFwdRowsF32 = 128;
 constexpr int kBwdKeysBf16 = 128;  // key rows per backward workgroup (4 waves x 32)
 constexpr int kBwdKeysF32 = 128;

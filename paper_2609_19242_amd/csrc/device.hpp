@@ -40,6 +40,10 @@ __device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t b
   return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 0));
 }
 
+__device__ __forceinline__ float buf_load_f32(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, byte_off, 0, 0));
+}
+
 // Transposed 8-byte LDS read (see the header comment).  p must point into LDS.
 __device__ __forceinline__ bf16x4 lds_read_tr(const bf16* p) {
   typedef __attribute__((address_space(3))) short4_t lds_s4;
@@ -63,4 +67,12 @@ __device__ __forceinline__ float exp2f_fast(float x) { return __builtin_amdgcn_e
 
 __device__ __forceinline__ bf16 to_bf16(float x) { return (bf16)x; }
 
+}  // namespace bdlm
+
+namespace bdlm {
+// fp32 atomic add through a buffer resource: offsets past the resource's end
+// are dropped by the hardware, so callers need no per-lane bounds branch.
+__device__ __forceinline__ void buf_atomic_add(__amdgpu_buffer_rsrc_t r, uint32_t byte_off, float v) {
+  __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(v, r, byte_off, 0, 0);
+}
 }  // namespace bdlm

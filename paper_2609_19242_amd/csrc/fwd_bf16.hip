@@ -19,8 +19,7 @@
 // (the rules in common.hpp).  Tiles inside every lane's interval run without a
 // mask test, tiles outside all of them are never visited, and the O(1) tiles
 // per range in between test each element against the lane's interval.
-#include "common.hpp"
-#include "device.hpp"
+#include "qtiles.hpp"
 
 namespace bdlm {
 
@@ -28,63 +27,10 @@ namespace {
 
 constexpr float kLn2 = 0.69314718055994530942f;
 
-struct FwdItem {
-  int b, h, r, t;
-};
-
-// Logical work id -> (batch, query head, query range, tile).  Logical ids are
-// grouped by KV head (so after xcd_remap one XCD serves one KV head and its L2
-// holds that head's K/V), the query heads of a group are interleaved, and the
-// tiles of each range run from the last (longest prefix) to the first.
-__device__ inline FwdItem fwd_item(const AttnArgs& a, int logical) {
-  const int per_kv = a.group * a.total_tiles;
-  const int bk = logical / per_kv;
-  const int rank = logical - bk * per_kv;
-  FwdItem it;
-  it.b = bk / a.kv_heads;
-  const int kvh = bk - it.b * a.kv_heads;
-  const int order = rank / a.group;
-  it.h = kvh * a.group + (rank - order * a.group);
-  if (a.interleave) {
-    it.r = order % a.n_q;
-    it.t = a.qr[it.r].ntiles - 1 - order / a.n_q;
-  } else {
-    int r = 0;
-    while (r + 1 < a.n_q && order >= a.qr[r + 1].tile0) ++r;
-    it.r = r;
-    it.t = a.qr[r].ntiles - 1 - (order - a.qr[r].tile0);
-  }
-  return it;
-}
-
-// Key tiles [t0, t1) of key range j that any query position in [pq0, pq1]
-// can see, and the sub-span [f0, f1) every one of them sees completely.
-__device__ inline void tile_span(const AttnArgs& a, int j, int qs, int pq0, int pq1, int BN,
-                                 int& t0, int& t1, int& f0, int& f1) {
-  const KRangeArg& kr = a.kr[j];
-  int lo0, hi0, lo1, hi1;
-  key_interval(qs, pq0, kr.stream, a.M, a.intra, lo0, hi0);
-  key_interval(qs, pq1, kr.stream, a.M, a.intra, lo1, hi1);
-  const int u0 = imax(lo0 - kr.pos0, 0), u1 = imin(hi1 - kr.pos0, kr.len);
-  t0 = t1 = f0 = f1 = 0;
-  if (u1 <= u0) return;
-  t0 = u0 / BN;
-  t1 = (u1 + BN - 1) / BN;
-  const int i0 = imax(lo1 - kr.pos0, 0), i1 = imin(hi0 - kr.pos0, kr.len);
-  if (i1 > i0) {
-    f0 = (i0 + BN - 1) / BN;
-    f1 = i1 / BN;
-  }
-}
-
-template <int D, int NW>
+template <int D, int NW, bool HILO>
 __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
   constexpr int BM = NW * 32, BN = 64, PITCH = D + 16, KS = D / 16, DT = D / 32;
   constexpr int NT = NW * 64;
-  constexpr int CPR = D / 8;               // 16-byte chunks per row
-  constexpr int CHUNKS = BN * CPR;
-  constexpr int CPT = CHUNKS / NT;         // chunks per thread per tile
-  static_assert(CHUNKS % NT == 0, "tile chunks must divide evenly");
   constexpr int STAGE = 2 * BN * PITCH;    // K tile + V tile
   __shared__ __attribute__((aligned(16))) bf16 lds[2 * STAGE];
 
@@ -93,7 +39,7 @@ __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
   const int G = lane >> 4, sl = lane & 15;
 
   const int n_wg = a.total_tiles * a.heads * a.batch;
-  const FwdItem it = fwd_item(a, xcd_remap(blockIdx.x, n_wg));
+  const QTileItem it = q_tile_item(a, xcd_remap(blockIdx.x, n_wg));
   const QRangeArg& qr = a.qr[it.r];
   const int kvh = it.h / a.group;
   const int row0 = it.t * BM;
@@ -123,53 +69,14 @@ __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
 
   // Uniform iteration state over (key range j, tile t).
   int j = 0, t = 0, t1 = 0, f0 = 0, f1 = 0;
-  auto find_from = [&](int jj, int& jo, int& to, int& t1o, int& f0o, int& f1o) -> bool {
-    for (; jj < a.n_k; ++jj) {
-      int a0, a1, b0, b1;
-      tile_span(a, jj, qr.stream, pq0, pq1, BN, a0, a1, b0, b1);
-      if (a1 > a0) {
-        jo = jj; to = a0; t1o = a1; f0o = b0; f1o = b1;
-        return true;
-      }
-    }
-    return false;
-  };
-  bool have = find_from(0, j, t, t1, f0, f1);
-
-  u32x4 pk[CPT], pv[CPT];
-  auto load_tile = [&](int jj, int tt) {
-    const KRangeArg& kr = a.kr[jj];
-    const int nrows = imin(BN, kr.len - tt * BN);
-    const int64_t eoff = (((int64_t)it.b * kr.bstride + (int64_t)tt * BN) * HKV + kvh) * D;
-    const uint32_t bytes = (uint32_t)(((int64_t)(nrows - 1) * HKV * D + D) * 2);
-    const auto rk = make_rsrc((const bf16*)kr.k + eoff, bytes);
-    const auto rv = make_rsrc((const bf16*)kr.v + eoff, bytes);
-#pragma unroll
-    for (int n = 0; n < CPT; ++n) {
-      const int cidx = tid + n * NT;
-      const int row = cidx / CPR, col = cidx % CPR;
-      const uint32_t off = (uint32_t)(((int64_t)row * HKV * D + col * 8) * 2);
-      pk[n] = buf_load16(rk, off);
-      pv[n] = buf_load16(rv, off);
-    }
-  };
-  auto store_tile = [&](int stage) {
-    bf16* ks = lds + stage * STAGE;
-    bf16* vs = ks + BN * PITCH;
-#pragma unroll
-    for (int n = 0; n < CPT; ++n) {
-      const int cidx = tid + n * NT;
-      const int row = cidx / CPR, col = cidx % CPR;
-      *(u32x4*)(ks + row * PITCH + col * 8) = pk[n];
-      *(u32x4*)(vs + row * PITCH + col * 8) = pv[n];
-    }
-  };
+  bool have = find_key_tile(a, 0, qr.stream, pq0, pq1, BN, j, t, t1, f0, f1);
+  KVTileLoader<D, BN, NT> ld;
 
   int cur = 0;
   int lane_lo = 0, lane_w = 0, lane_j = -1;
   if (have) {
-    load_tile(j, t);
-    store_tile(0);
+    ld.load(a, j, t, it.b, kvh, tid);
+    ld.template store<PITCH>(lds, lds + BN * PITCH, tid);
   }
   __syncthreads();
 
@@ -177,17 +84,11 @@ __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
     // Next tile (possibly in a later key range), prefetched into registers.
     int jn = j, tn = t + 1, t1n = t1, f0n = f0, f1n = f1;
     bool have_next = tn < t1;
-    if (!have_next) have_next = find_from(j + 1, jn, tn, t1n, f0n, f1n);
-    if (have_next) load_tile(jn, tn);
+    if (!have_next) have_next = find_key_tile(a, j + 1, qr.stream, pq0, pq1, BN, jn, tn, t1n, f0n, f1n);
+    if (have_next) ld.load(a, jn, tn, it.b, kvh, tid);
 
     if (lane_j != j) {  // this lane's visible key interval inside range j
-      const KRangeArg& kr = a.kr[j];
-      int lo, hi;
-      key_interval(qr.stream, pq, kr.stream, a.M, a.intra, lo, hi);
-      lo = imax(lo, kr.pos0);
-      hi = imin(hi, kr.pos0 + kr.len);
-      lane_lo = lo;
-      lane_w = imax(hi - lo, 0);
+      lane_key_interval(a, j, qr.stream, pq, lane_lo, lane_w);
       lane_j = j;
     }
 
@@ -224,14 +125,16 @@ __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
     const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
     const float alpha = exp2f_fast(m_run - m_use);
     float psum = 0.f;
-    bf16x8 pb[4];
+    bf16x8 pb[4], pl[4];
 #pragma unroll
     for (int u = 0; u < 2; ++u)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const float p = exp2f_fast(fmaf(sacc[u][i], c, -m_use));
         psum += p;
-        pb[u * 2 + (i >> 3)][i & 7] = to_bf16(p);
+        const bf16 hi = to_bf16(p);
+        pb[u * 2 + (i >> 3)][i & 7] = hi;
+        if constexpr (HILO) pl[u * 2 + (i >> 3)][i & 7] = to_bf16(p - (float)hi);
       }
     l_run = l_run * alpha + psum;
     m_run = m_new;
@@ -249,10 +152,11 @@ __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
       for (int d = 0; d < DT; ++d) {
         const bf16x8 va = cat(lds_read_tr(vp + 32 * d), lds_read_tr(vp + 32 * d + 8 * PITCH));
         acc[d] = mfma32(va, pb[u], acc[d]);
+        if constexpr (HILO) acc[d] = mfma32(va, pl[u], acc[d]);
       }
     }
 
-    if (have_next) store_tile(cur ^ 1);
+    if (have_next) ld.template store<PITCH>(lds + (cur ^ 1) * STAGE, lds + (cur ^ 1) * STAGE + BN * PITCH, tid);
     __syncthreads();
     cur ^= 1;
     j = jn; t = tn; t1 = t1n; f0 = f0n; f1 = f1n;
@@ -300,10 +204,13 @@ hipError_t launch_fwd_bf16(const AttnArgs& a, int head_dim, hipStream_t s) {
   constexpr int NW = kFwdRowsBf16 / 32;
   const int n = a.total_tiles * a.heads * a.batch;
   if (n == 0) return hipSuccess;
-  if (head_dim == 128)
-    hipLaunchKernelGGL((fwd_bf16_kernel<128, NW>), dim3(n), dim3(NW * 64), 0, s, a);
-  else
-    hipLaunchKernelGGL((fwd_bf16_kernel<64, NW>), dim3(n), dim3(NW * 64), 0, s, a);
+  if (head_dim == 128) {
+    if (a.hilo) hipLaunchKernelGGL((fwd_bf16_kernel<128, NW, true>), dim3(n), dim3(NW * 64), 0, s, a);
+    else hipLaunchKernelGGL((fwd_bf16_kernel<128, NW, false>), dim3(n), dim3(NW * 64), 0, s, a);
+  } else {
+    if (a.hilo) hipLaunchKernelGGL((fwd_bf16_kernel<64, NW, true>), dim3(n), dim3(NW * 64), 0, s, a);
+    else hipLaunchKernelGGL((fwd_bf16_kernel<64, NW, false>), dim3(n), dim3(NW * 64), 0, s, a);
+  }
   return hipGetLastError();
 }
 

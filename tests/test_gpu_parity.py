@@ -20,22 +20,22 @@ pytestmark = pytest.mark.gpu
 DEV = "cuda"
 
 
-def run_joint(q, k, v, do, M, reading, out_f32):
+def run_joint(q, k, v, do, M, reading, out_f32, hilo=False):
     qd, kd, vd, dod = (t.to(DEV) for t in (q, k, v, do))
-    o, lse = bd.joint_fwd(qd, kd, vd, M, clean_intra=reading, out_f32=out_f32)
-    dq, dk, dv = bd.joint_bwd(qd, kd, vd, o, lse, dod, M, clean_intra=reading, out_f32=out_f32)
+    o, lse = bd.joint_fwd(qd, kd, vd, M, clean_intra=reading, out_f32=out_f32, hilo=hilo)
+    dq, dk, dv = bd.joint_bwd(qd, kd, vd, o, lse, dod, M, clean_intra=reading, out_f32=out_f32, hilo=hilo)
     torch.cuda.synchronize()
     return o, lse, dq, dk, dv
 
 
-def check_joint(q, k, v, do, M, reading, dtype, heads=None, tag="", out_f32=True):
+def check_joint(q, k, v, do, M, reading, dtype, heads=None, tag="", out_f32=True, hilo=False):
     """GPU joint fwd+bwd against the oracle on the query heads ``heads`` (all by default).
 
     Strict tolerance on fp32 outputs; with bf16 outputs (``out_f32=False``) the
     bound adds the output rounding.
     """
     L = q.shape[1] // 2
-    o, lse, dq, dk, dv = run_joint(q, k, v, do, M, reading, out_f32)
+    o, lse, dq, dk, dv = run_joint(q, k, v, do, M, reading, out_f32, hilo)
     hs = list(range(q.shape[2])) if heads is None else heads
     O, LSE = oracle.joint_fwd(q, k, v, L, M, clean_intra=reading, heads=hs)
     dQ, dK, dV = oracle.joint_bwd(q, k, v, O, LSE, do[:, :, hs], L, M, clean_intra=reading, heads=hs)
@@ -62,14 +62,15 @@ SMALL = [
 ]
 
 
-@pytest.mark.parametrize("mode", ["bf16", "bf16-out-bf16", "fp32"])
+@pytest.mark.parametrize("mode", ["bf16", "bf16-out-bf16", "bf16-hilo", "fp32"])
 @pytest.mark.parametrize("reading", [0, 1], ids=["causal", "block"])
 @pytest.mark.parametrize("shape", SMALL, ids=lambda s: "L{}-M{}-H{}x{}-d{}-b{}".format(*s))
 def test_joint_small(shape, reading, mode):
     L, M, Hq, Hkv, D, B = shape
     dtype = torch.float32 if mode == "fp32" else torch.bfloat16
     q, k, v, do = joint_inputs(L, Hq, Hkv, D, dtype, batch=B, seed=L + M + D)
-    check_joint(q, k, v, do, M, reading, dtype, tag=f"L{L} M{M} r{reading}", out_f32=(mode != "bf16-out-bf16"))
+    check_joint(q, k, v, do, M, reading, dtype, tag=f"L{L} M{M} r{reading}", out_f32=(mode != "bf16-out-bf16"),
+                hilo=(mode == "bf16-hilo"))
 
 
 @pytest.mark.parametrize("reading", [0, 1], ids=["causal", "block"])

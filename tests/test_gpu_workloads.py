@@ -52,12 +52,12 @@ def dv_identity(dv, do, group, tag):
     assert err < 5e-3, err
 
 
-def joint_check(w, reading=0, n_random=24):
+def joint_check(w, reading=0, n_random=24, hilo=False):
     L, M = w.L, w.block_size
     torch.cuda.empty_cache()
     q, k, v, do = synth.make_joint(w, device=DEV)
-    o, lse = bd.joint_fwd(q, k, v, M, clean_intra=reading, out_f32=True)
-    dq, dk, dv = bd.joint_bwd(q, k, v, o, lse, do, M, clean_intra=reading, out_f32=True)
+    o, lse = bd.joint_fwd(q, k, v, M, clean_intra=reading, out_f32=True, hilo=hilo)
+    dq, dk, dv = bd.joint_bwd(q, k, v, o, lse, do, M, clean_intra=reading, out_f32=True, hilo=hilo)
     torch.cuda.synchronize()
     tag = w.name
     assert torch.isfinite(o).all() and torch.isfinite(lse).all()
@@ -110,7 +110,10 @@ def test_workload_32k_block_reading():
 
 
 def test_workload_128k():
-    joint_check(WORKLOADS["128k"], 0, n_random=8)
+    # 1% of the keys are scaled x8: a single bf16 term for P and dS leaves ~7e-2
+    # in dQ (through dS K and through D = rowsum(dO O)), so P and dS enter their
+    # products as bf16 hi + lo.
+    joint_check(WORKLOADS["128k"], 0, n_random=8, hilo=True)
 
 
 def csbp_ranges(w):
