@@ -240,6 +240,8 @@ def main():
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-csbp", action="store_true")
+    ap.add_argument("--pmc-pass", action="store_true",
+                    help="one 32K fwd+bwd step and a plain 1 GiB device copy, for rocprofv3 counter runs")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -255,6 +257,16 @@ def main():
         sys.exit(1)
     bd.lib()  # fail loudly if the HIP library is missing
 
+    if args.pmc_pass:
+        # Counter runs: one warm step of every kernel, then a plain copy of known
+        # size (2^30 bytes read, 2^30 written) that calibrates FETCH_SIZE / WRITE_SIZE.
+        bench_32k(torch, bd, synth, 1, 1)
+        src = torch.empty(1 << 29, dtype=torch.bfloat16, device="cuda").fill_(1.0)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print("[bench] pmc pass done", flush=True)
+        return
     main_res = bench_32k(torch, bd, synth, args.steps, args.warmup)
     print(f"[bench] 32k: {main_res['ms_per_step']:.3f} ms/step, {main_res['value']:.1f} useful TFLOP/s", flush=True)
     csbp = None if args.no_csbp else bench_csbp(torch, bd, synth, max(2, args.steps // 2), 1)
