@@ -154,8 +154,10 @@ bdlm_status bdlm_lse_merge(int64_t batch, int64_t rows, int32_t heads, int32_t h
                            const float* const* lse_parts, int32_t part_dtype,
                            void* o, float* lse, int32_t out_dtype, hipStream_t stream);
 
-/* Workspace bytes bdlm_attn_bwd needs for these query ranges: the fp32 row
- * dots D = rowsum(dO * O), batch * len * heads floats per range. */
+/* Workspace bytes bdlm_attn_bwd needs for these query ranges: per range two
+ * fp32 arrays of batch * len * heads values (each rounded up to 256 bytes),
+ * LSE * log2(e) and the row dots D = rowsum(dO * O).  Ranges whose
+ * batch * len * heads exceeds 2^28 are rejected by bdlm_attn_bwd. */
 size_t bdlm_attn_bwd_workspace_bytes(const bdlm_problem* p, int32_t n_q, const bdlm_range* q_ranges);
 
 /*

@@ -19,6 +19,8 @@ OUT = os.path.join(HERE, "libbdlm_attn.so")
 BUILD_DIR = os.path.join(HERE, "_build")
 SOURCES = ["api.cpp", "fwd_bf16.hip", "fwd_f32.hip", "merge.hip", "bwd_pre.hip", "bwd_bf16.hip", "bwd_dq.hip", "bwd_f32.hip"]
 ARCH = os.environ.get("BDLM_OFFLOAD_ARCH", "gfx950")
+# Per-source code-generation options (none at present).
+EXTRA_FLAGS: dict = {}
 
 
 def hipcc() -> str:
@@ -39,7 +41,7 @@ def flags() -> list:
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ".o")
-    cmd = [hipcc(), *flags(), "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [hipcc(), *flags(), *EXTRA_FLAGS.get(src, []), "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
     res = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{res.stdout}")

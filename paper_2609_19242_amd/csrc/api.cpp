@@ -285,7 +285,7 @@ size_t bdlm_attn_bwd_workspace_bytes(const bdlm_problem* p, int32_t n_q, const b
   size_t tot = 0;
   for (int i = 0; i < n_q; ++i) {
     const size_t rows = (size_t)p->batch * (size_t)(q_ranges[i].len > 0 ? q_ranges[i].len : 0);
-    tot += align256(rows * p->heads * sizeof(float));  // D = rowsum(dO * O)
+    tot += 2 * align256(rows * p->heads * sizeof(float));  // LSE * log2(e), then D = rowsum(dO * O)
   }
   return tot;
 }
@@ -326,8 +326,13 @@ bdlm_status bdlm_attn_bwd(const bdlm_problem* p, int32_t n_q, const bdlm_range* 
     a.qr[i].dO = dO[i];
     a.qr[i].dq = dq[i];
     const size_t rows = (size_t)p->batch * (size_t)r.len;
-    a.qr[i].delta = reinterpret_cast<float*>(ws);
-    ws += align256(rows * p->heads * sizeof(float));
+    const size_t arr = align256(rows * p->heads * sizeof(float));
+    if (arr > ((size_t)1 << 30))
+      return fail(BDLM_ERR_UNSUPPORTED, "query range %d: batch * len * heads = %zu rows exceeds 2^28", i,
+                  rows * p->heads);
+    a.qr[i].l2 = reinterpret_cast<float*>(ws);
+    a.qr[i].delta = reinterpret_cast<float*>(ws + arr);
+    ws += 2 * arr;
   }
   for (int j = 0; j < n_k; ++j) {
     if ((st = check_range(p, k_ranges[j], "key", j)) != BDLM_OK) return st;

@@ -10,14 +10,15 @@
 //
 // A workgroup owns 128 keys of one KV head (4 waves x 32 keys), holds their K
 // and V rows in registers as MFMA operands and accumulates dK^T and dV^T in
-// registers for the whole pass.  It walks the query heads of the group and,
-// for each query range, the 32-row query steps that can see its keys (the
-// query-side intervals of common.hpp give the span in closed form; steps every
-// key sees completely skip the mask test).  Per step and wave:
+// registers for the whole pass.  It walks the 32-row query steps that can see
+// its keys, from the end of the query ranges down, and at each step every
+// query range and every pair of query heads of the group (steps every key sees
+// completely skip the mask test).  Per step and wave:
 //   S = Q K^T, dP = dO V^T          (Q, dO rows from LDS as A, K, V from registers as B)
 //   dV^T += dO^T P, dK^T += Q^T dS  (dO^T, Q^T via LDS transpose reads; P, dS from registers)
-// Q/dO/LSE/D of the next step are prefetched into registers at the top of the
-// step and stored to the other LDS stage in its middle; one barrier per step.
+// A step's Q, dO, LSE*log2(e) and D go from global memory straight into one of
+// three LDS stages (no register staging), two steps ahead of their use; one
+// barrier per step.
 #include "common.hpp"
 #include "device.hpp"
 
@@ -25,23 +26,49 @@ namespace bdlm {
 
 namespace {
 
-constexpr float kLog2e = 1.44269504088896340736f;
+template <int D, int NH>
+struct BwdStage {
+  static constexpr int PITCH = D + 16;  // LDS row pitch in elements (two 16-byte pad slots)
+  bf16 q[NH * 32 * PITCH];
+  bf16 dO[NH * 32 * PITCH];
+  float l2[64];  // [head][row]: LSE * log2(e)  (64 floats: one copy instruction)
+  float dl[64];  // [head][row]: D
+};
 
-// NH query heads of the GQA group are processed per step (same 32 query
-// rows): their products and softmax are independent instruction streams the
-// scheduler interleaves, so one head's MFMAs run while the other's VALU work
-// issues -- with a single wave per SIMD nothing else could fill those gaps.
+// Global -> LDS copy plan of one step.  Each tensor (Q, dO) of a stage is
+// NH * 32 rows of PITCH / 8 16-byte slots; a copy instruction fills 64
+// consecutive slots (one per lane) and the pad slots get an out-of-range
+// offset.  Tensor instructions g = 0 .. 2 TI - 1 go to wave g % 4; waves 2
+// and 3 copy the LSE*log2(e) and D rows (one dword instruction each).  NMIN is
+// the smallest per-wave instruction count of a step: waiting
+// for vmcnt <= NMIN after issuing the next step leaves only that step's copies
+// in flight.
+template <int D, int NH>
+struct CopyPlan {
+  static constexpr int SLOTS = BwdStage<D, NH>::PITCH / 8;
+  static constexpr int TI = NH * 32 * SLOTS / 64;
+  static constexpr int IPW = (2 * TI + 3) / 4;
+  static constexpr int count(int w) { return (2 * TI - w + 3) / 4 + (w >= 2 ? 1 : 0); }
+  static constexpr int NMIN = count(0) < count(1) ? (count(0) < count(2) ? (count(0) < count(3) ? count(0) : count(3))
+                                                                         : (count(2) < count(3) ? count(2) : count(3)))
+                                                  : (count(1) < count(2) ? (count(1) < count(3) ? count(1) : count(3))
+                                                                         : (count(2) < count(3) ? count(2) : count(3)));
+  static_assert((NH * 32 * SLOTS) % 64 == 0, "whole copy instructions per tensor");
+};
+
+constexpr uint32_t kOutOfRange = 0x7fff0000u;
+
 template <int D, bool HILO, int NH>
 __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
-  constexpr int BN = kBwdKeysBf16, BM = 32, PITCH = D + 16, KS = D / 16, DT = D / 32, NT = 256;
-  constexpr int CPR = D / 8;
-  constexpr int QCPT = NH * BM * CPR / NT;  // 16-byte chunks per thread per tensor and step
-  static_assert(BN == 128 && (NH * BM * CPR) % NT == 0, "tile shape");
-  __shared__ __attribute__((aligned(16))) bf16 q_lds[2][NH][BM * PITCH];
-  __shared__ __attribute__((aligned(16))) bf16 do_lds[2][NH][BM * PITCH];
-  __shared__ __attribute__((aligned(16))) float st_lds[2][NH][2][BM];  // [stage][head][lse*log2e | D][row]
+  constexpr int BN = kBwdKeysBf16, BM = 32, KS = D / 16, DT = D / 32;
+  using Stage = BwdStage<D, NH>;
+  using Plan = CopyPlan<D, NH>;
+  constexpr int PITCH = Stage::PITCH;
+  static_assert(BN == 128, "tile shape");
+  __shared__ __attribute__((aligned(16))) Stage stages[3];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, half = lane >> 5;
   const int G = lane >> 4, sl = lane & 15;
   const int64_t H = a.heads, HKV = a.kv_heads;
@@ -96,135 +123,139 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
       dva[d][i] = 0.f;
     }
 
-  // ---- iteration: query ranges (outer), query heads of the group, 32-row steps.
-  // The span of steps that can see this tile's keys depends only on the range.
-  auto span = [&](int qi, int& s0, int& s1, int& f0, int& f1) -> bool {
-    const QRangeArg& qr = a.qr[qi];
+  // ---- iteration order.  Per query range, the 32-row steps that can see this
+  // tile's keys form a span [s0, s1) (the query-side intervals of common.hpp
+  // give it in closed form) with a sub-span [f0, f1) that every key sees
+  // completely.  Steps are walked from the highest index down; at each index
+  // every range active there is visited (in range order), and in each range
+  // every pair of query heads.  Visible query rows extend to the end of a range
+  // for every key tile, so all workgroups resident on an XCD start on the same
+  // rows and stay close together: their Q/dO reads are shared in L2.
+  // Per range: steps [s0, s1), fully visible steps [f0, f1), and the queries
+  // [qa, qa + qw) of the range that see this lane's key.  Four named slots
+  // (not an array) so that every field stays in registers.
+  struct Span {
+    int s0, s1, f0, f1, pos0, qa, qw;
+  };
+  auto make_span = [&](int q) -> Span {
+    Span sp{0, 0, 0, 0, 0, 0, 0};
+    if (q >= a.n_q) return sp;
+    const QRangeArg& qr = a.qr[q];
+    sp.pos0 = qr.pos0;
     int lo0, hi0, lo1, hi1;
     query_interval(qr.stream, kr.stream, kpos_first, a.M, a.intra, lo0, hi0);
     query_interval(qr.stream, kr.stream, kpos_last, a.M, a.intra, lo1, hi1);
     const int u0 = imax(lo0 - qr.pos0, 0), u1 = imin(hi1 - qr.pos0, qr.len);
-    if (u1 <= u0) return false;
-    s0 = u0 / BM;
-    s1 = (u1 + BM - 1) / BM;
-    const int i0 = imax(lo1 - qr.pos0, 0), i1 = imin(hi0 - qr.pos0, qr.len);
-    f0 = f1 = 0;
-    if (i1 > i0 && !ragged) {
-      f0 = (i0 + BM - 1) / BM;
-      f1 = i1 / BM;
-    }
-    return true;
-  };
-  auto first_range = [&](int qi, int& qo, int& s0, int& s1, int& f0, int& f1) -> bool {
-    for (; qi < a.n_q; ++qi)
-      if (span(qi, s0, s1, f0, f1)) {
-        qo = qi;
-        return true;
+    if (u1 > u0) {
+      sp.s0 = u0 / BM;
+      sp.s1 = (u1 + BM - 1) / BM;
+      const int i0 = imax(lo1 - qr.pos0, 0), i1 = imin(hi0 - qr.pos0, qr.len);
+      if (i1 > i0 && !ragged) {
+        sp.f0 = (i0 + BM - 1) / BM;
+        sp.f1 = i1 / BM;
       }
-    return false;
+    }
+    int lo, hi;
+    query_interval(qr.stream, kr.stream, pk, a.M, a.intra, lo, hi);
+    lo = imax(lo, qr.pos0);
+    hi = imin(hi, qr.pos0 + qr.len);
+    sp.qa = lo;
+    sp.qw = key_ok ? imax(hi - lo, 0) : 0;
+    return sp;
   };
-
-  // Prefetch registers of the next step: Q and dO rows of the NH heads (the
-  // heads are adjacent in memory, so a step's rows are NH*D contiguous
-  // elements), and each lane's row's raw LSE and D for every head.
-  u32x4 pq[QCPT], pdo[QCPT];
-  float pz[NH], pd[NH];
-  int prow_ok = 0;
-  auto load_step = [&](int qi, int hp, int step) {
-    const QRangeArg& qr = a.qr[qi];
-    const int h0 = kvh * a.group + hp * NH;
-    const int row0 = step * BM;
-    const int nrows = imin(BM, qr.len - row0);
-    const int64_t qoff = (((int64_t)b * qr.bstride + row0) * H + h0) * D;
-    const uint32_t bytes = (uint32_t)(((int64_t)(nrows - 1) * H * D + NH * D) * 2);
-    const auto rq = make_rsrc((const bf16*)qr.q + qoff, bytes);
-    const auto rdo = make_rsrc((const bf16*)qr.dO + qoff, bytes);
-#pragma unroll
-    for (int n = 0; n < QCPT; ++n) {
-      const int cidx = tid + n * NT;
-      const int row = cidx / (NH * CPR), col = cidx % (NH * CPR);
-      const uint32_t off = (uint32_t)(((int64_t)row * H * D + col * 8) * 2);
-      pq[n] = buf_load16(rq, off);
-      pdo[n] = buf_load16(rdo, off);
-    }
-#pragma unroll
-    for (int j = 0; j < NH; ++j) {
-      const auto rl = make_rsrc(qr.lse + ((int64_t)b * H + h0 + j) * qr.bstride + row0, (uint32_t)nrows * 4);
-      const auto rd = make_rsrc(qr.delta + ((int64_t)b * H + h0 + j) * qr.len + row0, (uint32_t)nrows * 4);
-      pz[j] = buf_load_f32(rl, (uint32_t)(tid & (BM - 1)) * 4);
-      pd[j] = buf_load_f32(rd, (uint32_t)(tid & (BM - 1)) * 4);
-    }
-    prow_ok = (tid & (BM - 1)) < nrows;
+  static_assert(kMaxQ == 4, "four range slots");
+  const Span R0 = make_span(0), R1 = make_span(1), R2 = make_span(2), R3 = make_span(3);
+  // Select by value (a select of member addresses would force the spans into memory).
+  auto sel4 = [](int q, int v0, int v1, int v2, int v3) { return q == 0 ? v0 : q == 1 ? v1 : q == 2 ? v2 : v3; };
+#define BDLM_PICK(f, q) sel4((q), R0.f, R1.f, R2.f, R3.f)
+  auto active = [](const Span& sp, int s) { return sp.s0 <= s && s < sp.s1; };
+  // First range after q that is active at step s (kMaxQ if none).
+  auto range_at = [&](int s, int q) -> int {
+    return (q < 0 && active(R0, s)) ? 0 : (q < 1 && active(R1, s)) ? 1
+         : (q < 2 && active(R2, s)) ? 2 : (q < 3 && active(R3, s)) ? 3 : kMaxQ;
   };
-  auto store_step = [&](int stage) {
-#pragma unroll
-    for (int n = 0; n < QCPT; ++n) {
-      const int cidx = tid + n * NT;
-      const int row = cidx / (NH * CPR), col = cidx % (NH * CPR);
-      const int j = col / CPR, cc = col % CPR;
-      *(u32x4*)(&q_lds[stage][j][row * PITCH + cc * 8]) = pq[n];
-      *(u32x4*)(&do_lds[stage][j][row * PITCH + cc * 8]) = pdo[n];
-    }
-    // Rows past the range end and rows that see no key get LSE = +inf (P = 0) and D = 0.
-#pragma unroll
-    for (int j = 0; j < NH; ++j) {
-      if (tid < BM) st_lds[stage][j][0][tid] = (prow_ok && pz[j] != -INFINITY) ? pz[j] * kLog2e : INFINITY;
-      else if (tid < 2 * BM) st_lds[stage][j][1][tid - BM] = prow_ok ? pd[j] : 0.f;
-    }
+  // Highest step below s that some range covers (-1 if none).
+  auto below = [](const Span& sp, int s) {
+    const int cand = imin(s - 1, sp.s1 - 1);
+    return cand >= sp.s0 ? cand : -1;
   };
-
+  auto step_below = [&](int s) -> int {
+    return imax(imax(below(R0, s), below(R1, s)), imax(below(R2, s), below(R3, s)));
+  };
+  // A cursor is (range, head pair, step); step < 0 once the walk is over.
+  struct Cursor {
+    int q, hp, s;
+  };
   const int npairs = a.group / NH;
-  int qi = 0, hp = 0, s = 0, s0 = 0, s1 = 0, f0 = 0, f1 = 0;
-  bool have = first_range(0, qi, s0, s1, f0, f1);
-  s = s0;
-  if (have) {
-    load_step(qi, hp, s);
-    store_step(0);
+  auto advance = [&](Cursor c) __attribute__((always_inline)) -> Cursor {
+    if (c.s < 0) return c;
+    if (++c.hp < npairs) return c;
+    c.hp = 0;
+    const int qn = range_at(c.s, c.q);
+    if (qn != kMaxQ) {
+      c.q = qn;
+      return c;
+    }
+    c.s = step_below(c.s);
+    c.q = c.s >= 0 ? range_at(c.s, -1) : 0;
+    return c;
+  };
+
+  // ---- copy plan: per-lane global offsets of this wave's tensor instructions
+  // (constant over the walk; the step moves the resource base).
+  uint32_t voff[Plan::IPW];
+#pragma unroll
+  for (int i = 0; i < Plan::IPW; ++i) {
+    const int g = 4 * i + w;
+    const int slot = (g % Plan::TI) * 64 + lane;
+    const int row = slot / Plan::SLOTS, ch = slot % Plan::SLOTS;
+    const int j = row / BM, rr = row % BM;
+    voff[i] = (g < 2 * Plan::TI && ch < D / 8) ? (uint32_t)(((rr * H + j) * D + ch * 8) * 2) : kOutOfRange;
   }
-  __syncthreads();
+  // Issue the copies of step c into stage S (an empty copy when c is past the end).
+  auto copy_step = [&](Stage& S, const Cursor c) __attribute__((always_inline)) {
+    const bool live = c.s >= 0;
+    const QRangeArg& qr = a.qr[live ? c.q : 0];
+    const int h0 = kvh * a.group + c.hp * NH;
+    const int row0 = c.s * BM;
+    const int nrows = live ? imin(BM, qr.len - row0) : 0;
+    const int64_t qoff = (((int64_t)b * qr.bstride + row0) * H + h0) * D;
+    const uint32_t qbytes = live ? (uint32_t)(((int64_t)(nrows - 1) * H + NH) * D * 2) : 0u;
+    const auto rq = make_rsrc((const bf16*)qr.q + (live ? qoff : 0), qbytes);
+    const auto rdo = make_rsrc((const bf16*)qr.dO + (live ? qoff : 0), qbytes);
+#pragma unroll
+    for (int i = 0; i < Plan::IPW; ++i) {
+      const int g = 4 * i + w;
+      if (g < Plan::TI) buf_to_lds<16>(rq, S.q + g * 512, voff[i], 0);
+      else if (g < 2 * Plan::TI) buf_to_lds<16>(rdo, S.dO + (g - Plan::TI) * 512, voff[i], 0);
+    }
+    if (w >= 2) {
+      // LSE*log2(e) (wave 2) or D (wave 3) of the NH heads' rows, [head][row]
+      // floats.  Each resource ends with its array, so rows past the end of the
+      // last head read zeros; other rows past the range end read finite values
+      // of the next head (those rows are always masked).
+      const int64_t loff = ((int64_t)b * H + h0) * qr.len + row0;
+      const int64_t total = (int64_t)a.batch * H * qr.len;
+      const uint32_t lbytes = live ? (uint32_t)((total - loff) * 4) : 0u;
+      const auto rl = make_rsrc((w == 2 ? qr.l2 : qr.delta) + (live ? loff : 0), lbytes);
+      const uint32_t vo = NH == 2 ? (uint32_t)(((lane >> 5) * qr.len + (lane & 31)) * 4) : (uint32_t)(lane * 4);
+      buf_to_lds<4>(rl, w == 2 ? S.l2 : S.dl, vo, 0);
+    }
+  };
 
-  // One barrier per step: Q/dO/LSE/D of step n+1 are stored to the other
-  // stage during step n; that stage was last read before the previous barrier.
-  int cur = 0, lane_range = -1, lane_qa = 0, lane_qw = 0;
   const float c = a.scale_log2;
-  while (have) {
-    int qin = qi, hpn = hp, sn = s + 1, s0n = s0, s1n = s1, f0n = f0, f1n = f1;
-    bool have_next = true;
-    if (sn >= s1) {
-      if (hp + 1 < npairs) {
-        hpn = hp + 1;
-        sn = s0;
-      } else {
-        hpn = 0;
-        have_next = first_range(qi + 1, qin, s0n, s1n, f0n, f1n);
-        sn = s0n;
-      }
-    }
-    // Unconditional prefetch (the last step re-reads its own rows) keeps the
-    // loads at the top of the step, a full step ahead of their LDS store.
-    if (have_next) load_step(qin, hpn, sn);
-    else load_step(qi, hp, s);
+  // One step of the walk on stage S: S = Q K^T, dP = dO V^T, P, dS, then
+  // dV^T += dO^T P, dK^T += Q^T dS for every head of the pair.
+  auto compute_step = [&](const Stage& S, const Cursor cu) __attribute__((always_inline)) {
+    const bool partial = !(cu.s >= BDLM_PICK(f0, cu.q) && cu.s < BDLM_PICK(f1, cu.q));
+    const int mbase = BDLM_PICK(pos0, cu.q) + cu.s * BM + 4 * half - BDLM_PICK(qa, cu.q);
+    const int lane_qw = BDLM_PICK(qw, cu.q);
 
-    const QRangeArg& qr = a.qr[qi];
-    if (lane_range != qi) {  // queries of range qi that see this lane's key
-      int lo, hi;
-      query_interval(qr.stream, kr.stream, pk, a.M, a.intra, lo, hi);
-      lo = imax(lo, qr.pos0);
-      hi = imin(hi, qr.pos0 + qr.len);
-      lane_qa = lo;
-      lane_qw = key_ok ? imax(hi - lo, 0) : 0;
-      lane_range = qi;
-    }
-    const bool partial = !(s >= f0 && s < f1);
-    const int mbase = qr.pos0 + s * BM + 4 * half - lane_qa;
-    __builtin_amdgcn_sched_barrier(0);
-
-    // S = Q K^T and dP = dO V^T for this wave's 32 keys, every head.
     f32x16 sacc[NH], dpacc[NH];
 #pragma unroll
     for (int j = 0; j < NH; ++j) {
-      const bf16* qs = &q_lds[cur][j][0];
-      const bf16* dos = &do_lds[cur][j][0];
+      const bf16* qs = S.q + j * BM * PITCH;
+      const bf16* dos = S.dO + j * BM * PITCH;
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         sacc[j][i] = 0.f;
@@ -238,7 +269,8 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
     }
 
     // P = exp2(S c - LSE log2 e) and dS = P (dP - D) per head; the mask only
-    // on partly visible steps.
+    // on partly visible steps.  Rows past the range end read Q = dO = 0 and are
+    // always masked.
     bf16x8 pb[NH][2], pl[NH][2], dsb[NH][2], dsl[NH][2];
 #pragma unroll
     for (int j = 0; j < NH; ++j) {
@@ -249,8 +281,8 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
       }
 #pragma unroll
       for (int g4 = 0; g4 < 4; ++g4) {
-        const f32x4 l2 = *(const f32x4*)(&st_lds[cur][j][0][8 * g4 + 4 * half]);
-        const f32x4 dl = *(const f32x4*)(&st_lds[cur][j][1][8 * g4 + 4 * half]);
+        const f32x4 l2 = *(const f32x4*)(&S.l2[j * BM + 8 * g4 + 4 * half]);
+        const f32x4 dl = *(const f32x4*)(&S.dl[j * BM + 8 * g4 + 4 * half]);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int i = 4 * g4 + e;
@@ -270,8 +302,8 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
     // one head and one 16-query half at a time with its transposed fragments.
 #pragma unroll
     for (int j = 0; j < NH; ++j) {
-      const bf16* qs = &q_lds[cur][j][0];
-      const bf16* dos = &do_lds[cur][j][0];
+      const bf16* qs = S.q + j * BM * PITCH;
+      const bf16* dos = S.dO + j * BM * PITCH;
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         const int off = (16 * u + 4 * (G >> 1) + (sl >> 2)) * PITCH + 16 * (G & 1) + 4 * (sl & 3);
@@ -286,13 +318,35 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
         }
       }
     }
-    store_step(cur ^ 1);
+  };
 
-    __syncthreads();
-    cur ^= 1;
-    qi = qin; hp = hpn; s = sn; s0 = s0n; s1 = s1n; f0 = f0n; f1 = f1n;
-    have = have_next;
+  // ---- the walk: three LDS stages, copies two steps ahead.  At the barrier
+  // closing a step, every wave has waited for its copies of the next step
+  // (only the copies of the step after it stay in flight), and every wave has
+  // finished reading the stage the following step's copies overwrite.
+  Cursor c0;
+  c0.s = step_below(kBig);
+  c0.q = c0.s >= 0 ? range_at(c0.s, -1) : 0;
+  c0.hp = 0;
+  Cursor c1 = advance(c0), c2 = advance(c1);
+  copy_step(stages[0], c0);
+  copy_step(stages[1], c1);
+  vm_wait_barrier<Plan::NMIN>();
+  int cur = 0;
+  while (c0.s >= 0) {
+    const int nx2 = cur == 0 ? 2 : cur - 1;  // (cur + 2) % 3
+    copy_step(stages[nx2], c2);
+    compute_step(stages[cur], c0);
+    vm_wait_barrier<Plan::NMIN>();
+    cur = cur == 2 ? 0 : cur + 1;
+    c0 = c1;
+    c1 = c2;
+    c2 = advance(c2);
   }
+  // Copies still in flight target stages nobody reads; they must land before
+  // the workgroup's LDS is released.
+  __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
+#undef BDLM_PICK
 
   // ---- epilogue: dK = scale dK^T^T, dV (rounded to bf16); unseen keys get zeros
   if (key_ok) {

@@ -1,7 +1,9 @@
 // Backward pre-pass, gfx950 (an HBM-bound elementwise pass).
 //
 // D[b][h][row] = sum_d dO * O in fp32: the row dot the softmax gradient
-// dS = P * (dP - D) needs (arXiv 2609.19242 App. C reuses the saved O).
+// dS = P * (dP - D) needs (arXiv 2609.19242 App. C reuses the saved O), and
+// L2[b][h][row] = LSE * log2(e) (+inf for rows that see no key, so that
+// exp2(s - L2) is 0 for them), the form the dK/dV kernel stages into LDS.
 // One thread per 8 consecutive head_dim elements; the D/8 threads of one
 // (row, head) are adjacent lanes and reduce with cross-lane shuffles.
 #include "common.hpp"
@@ -51,7 +53,11 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(const AttnArgs a) {
 #pragma unroll
   for (int w = CPR / 2; w > 0; w >>= 1) s += __shfl_xor(s, w, CPR);
   if (!ok) return;
-  if (chunk == 0) qr.delta[(b * H + h) * qr.len + row] = s;
+  if (chunk == 0) {
+    const float z = qr.lse[(b * H + h) * qr.bstride + row];
+    qr.delta[(b * H + h) * qr.len + row] = s;
+    qr.l2[(b * H + h) * qr.len + row] = (z == -INFINITY) ? INFINITY : z * 1.44269504088896340736f;
+  }
 }
 
 int64_t max_q_threads(const AttnArgs& a, int cpr) {

@@ -79,6 +79,7 @@ struct QRangeArg {
   float* lse;
   const void* dO;
   void* dq;
+  float* l2;          // LSE * log2(e), +inf where LSE = -inf, [batch][heads][len]
   float* delta;       // D = rowsum(dO * O), [batch][heads][len]
 };
 

@@ -44,6 +44,27 @@ __device__ __forceinline__ float buf_load_f32(__amdgpu_buffer_rsrc_t r, uint32_t
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, byte_off, 0, 0));
 }
 
+// Global -> LDS copy that bypasses registers: lane i of the wave writes its
+// BYTES (4 or 16) to lds + i * BYTES (lds is wave-uniform); offsets past the
+// resource's end write zeros and fetch nothing.  Completion counts against
+// vmcnt like any vector-memory load.
+template <int BYTES>
+__device__ __forceinline__ void buf_to_lds(__amdgpu_buffer_rsrc_t r, void* lds, uint32_t voff, uint32_t soff) {
+  static_assert(BYTES == 4 || BYTES == 16, "LDS copy width");
+  auto* dst = (__attribute__((address_space(3))) void*)lds;
+  if constexpr (BYTES == 16) __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, voff, soff, 0, 0);
+  else __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 4, voff, soff, 0, 0);
+}
+
+// Wait until at most N vector-memory operations of this wave are in flight,
+// then a workgroup barrier.  Used where LDS written by buf_to_lds copies of
+// every wave must be complete; the memory clobber keeps LDS accesses on their
+// side of the barrier.
+template <int N>
+__device__ __forceinline__ void vm_wait_barrier() {
+  asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(N) : "memory");
+}
+
 // Transposed 8-byte LDS read (see the header comment).  p must point into LDS.
 __device__ __forceinline__ bf16x4 lds_read_tr(const bf16* p) {
   typedef __attribute__((address_space(3))) short4_t lds_s4;

@@ -91,7 +91,7 @@ def test_merge_and_bwd_validation():
     p = _prob()
     qr = [Range(CORRUPTED, 0, 64)]
     need = bd.attn_bwd_workspace_bytes(p, qr)
-    assert need == 256 * (-(-64 * 4 * 4 // 256))  # fp32 D per (row, head), 256-byte aligned
+    assert need == 2 * 256 * (-(-64 * 4 * 4 // 256))  # fp32 LSE*log2(e) and D per (row, head), 256-byte aligned
     f = bd._parr([FAKE])
     rc = L.bdlm_attn_bwd(ctypes.byref(p), 1, bd._rarr(qr), f, f, f, f, f, 1, bd._rarr([Range(CLEAN, 0, 64)]),
                          f, f, f, f, FAKE, need - 1, None)
