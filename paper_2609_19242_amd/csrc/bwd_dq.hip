@@ -21,9 +21,11 @@ constexpr float kLog2e = 1.44269504088896340736f;
 
 template <int D, int NW, bool HILO>
 __global__ __launch_bounds__(NW * 64) void bwd_dq_kernel(const AttnArgs a) {
-  constexpr int BM = NW * 32, BN = 64, PITCH = D + 16, KS = D / 16, DT = D / 32;
+  constexpr int BM = NW * 32, BN = 64, KS = D / 16, DT = D / 32;
+  // K and V row reads at pitch PB; K^T transpose reads from a second copy of K at pitch PT.
+  constexpr int PB = pitch_b128(D), PT = pitch_tr(D);
   constexpr int NT = NW * 64;
-  constexpr int STAGE = 2 * BN * PITCH;  // K tile + V tile
+  constexpr int STAGE = BN * (2 * PB + PT);  // K tile, V tile, K tile again
   __shared__ __attribute__((aligned(16))) bf16 lds[2 * STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -78,7 +80,7 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_kernel(const AttnArgs a) {
   int lane_lo = 0, lane_w = 0, lane_j = -1;
   if (have) {
     ld.load(a, j, t, it.b, kvh, tid);
-    ld.template store<PITCH>(lds, lds + BN * PITCH, tid);
+    ld.template store<PB, PB, PT>(lds, lds + BN * PB, tid, lds + 2 * BN * PB);
   }
   __syncthreads();
 
@@ -93,7 +95,8 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_kernel(const AttnArgs a) {
     }
 
     const bf16* Ks = lds + cur * STAGE;
-    const bf16* Vs = Ks + BN * PITCH;
+    const bf16* Vs = Ks + BN * PB;
+    const bf16* Kt = Ks + 2 * BN * PB;
     f32x16 sacc[2], dpacc[2];
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
@@ -102,8 +105,8 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_kernel(const AttnArgs a) {
         sacc[u][i] = 0.f;
         dpacc[u][i] = 0.f;
       }
-      const bf16* kp = Ks + (u * 32 + l32) * PITCH + 8 * half;
-      const bf16* vp = Vs + (u * 32 + l32) * PITCH + 8 * half;
+      const bf16* kp = Ks + (u * 32 + l32) * PB + 8 * half;
+      const bf16* vp = Vs + (u * 32 + l32) * PB + 8 * half;
 #pragma unroll
       for (int s = 0; s < KS; ++s) {
         sacc[u] = mfma32(*(const bf16x8*)(kp + 16 * s), qf[s], sacc[u]);
@@ -139,16 +142,19 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_kernel(const AttnArgs a) {
     // dQ^T[d][q] += sum_key K[key][d] dS[q][key]; key order per 16-key step as in the forward.
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      const bf16* kp = Ks + (16 * u + 4 * (G >> 1) + (sl >> 2)) * PITCH + 16 * (G & 1) + 4 * (sl & 3);
+      const bf16* kp = Kt + (16 * u + 4 * (G >> 1) + (sl >> 2)) * PT + 16 * (G & 1) + 4 * (sl & 3);
 #pragma unroll
       for (int d = 0; d < DT; ++d) {
-        const bf16x8 ka = cat(lds_read_tr(kp + 32 * d), lds_read_tr(kp + 32 * d + 8 * PITCH));
+        const bf16x8 ka = cat(lds_read_tr(kp + 32 * d), lds_read_tr(kp + 32 * d + 8 * PT));
         acc[d] = mfma32(ka, dsb[u], acc[d]);
         if constexpr (HILO) acc[d] = mfma32(ka, dsl[u], acc[d]);
       }
     }
 
-    if (have_next) ld.template store<PITCH>(lds + (cur ^ 1) * STAGE, lds + (cur ^ 1) * STAGE + BN * PITCH, tid);
+    if (have_next) {
+      bf16* st = lds + (cur ^ 1) * STAGE;
+      ld.template store<PB, PB, PT>(st, st + BN * PB, tid, st + 2 * BN * PB);
+    }
     __syncthreads();
     cur ^= 1;
     j = jn; t = tn; t1 = t1n; f0 = f0n; f1 = f1n;

@@ -13,7 +13,8 @@
 // two half-waves until the epilogue.  O^T += V^T P^T uses the probabilities
 // straight from the S^T registers as the B operand, and V^T fragments come
 // from the row-major V tile through LDS transpose reads.  K/V tiles are
-// double-buffered in LDS with one barrier per tile.
+// double-buffered in LDS with one barrier per tile, K and V at the row pitches
+// that make their row reads and transpose reads free of bank conflicts.
 //
 // Masking: each lane's visible keys in a key range are one position interval
 // (the rules in common.hpp).  Tiles inside every lane's interval run without a
@@ -26,12 +27,14 @@ namespace bdlm {
 namespace {
 
 constexpr float kLn2 = 0.69314718055994530942f;
+constexpr float kSlack = 8.f;  // largest exponent p = exp2(s c - m_run) may reach before m_run moves
 
 template <int D, int NW, bool HILO>
 __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
-  constexpr int BM = NW * 32, BN = 64, PITCH = D + 16, KS = D / 16, DT = D / 32;
+  constexpr int BM = NW * 32, BN = 64, KS = D / 16, DT = D / 32;
+  constexpr int PK = pitch_b128(D), PV = pitch_tr(D);  // K: row reads; V: transpose reads
   constexpr int NT = NW * 64;
-  constexpr int STAGE = 2 * BN * PITCH;    // K tile + V tile
+  constexpr int STAGE = BN * (PK + PV);  // K tile + V tile
   __shared__ __attribute__((aligned(16))) bf16 lds[2 * STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -76,7 +79,7 @@ __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
   int lane_lo = 0, lane_w = 0, lane_j = -1;
   if (have) {
     ld.load(a, j, t, it.b, kvh, tid);
-    ld.template store<PITCH>(lds, lds + BN * PITCH, tid);
+    ld.template store<PK, PV>(lds, lds + BN * PK, tid);
   }
   __syncthreads();
 
@@ -93,13 +96,13 @@ __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
     }
 
     const bf16* Ks = lds + cur * STAGE;
-    const bf16* Vs = Ks + BN * PITCH;
+    const bf16* Vs = Ks + BN * PK;
     f32x16 sacc[2];
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) sacc[u][i] = 0.f;
-      const bf16* kp = Ks + (u * 32 + l32) * PITCH + 8 * half;
+      const bf16* kp = Ks + (u * 32 + l32) * PK + 8 * half;
 #pragma unroll
       for (int s = 0; s < KS; ++s) sacc[u] = mfma32(*(const bf16x8*)(kp + 16 * s), qf[s], sacc[u]);
     }
@@ -121,9 +124,23 @@ __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[u][i]);
     mx = fmaxf(mx, partner(mx));
-    const float m_new = fmaxf(m_run, mx * c);
-    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-    const float alpha = exp2f_fast(m_run - m_use);
+    // Lazy rescaling: the running max m_run only moves when some lane's tile
+    // max exceeds it by more than kSlack (log2 units).  Otherwise the stale
+    // max stays, so p = exp2(s c - m_run) <= 2^kSlack: exact in fp32 and bf16,
+    // and l_run, O and the final LSE all use the same m_run.  The test is
+    // wave-uniform, so the O rescale (64 multiplies per lane) is skipped for
+    // the whole wave on most tiles.
+    if (__builtin_amdgcn_ballot_w64(mx * c > m_run + kSlack) != 0) {
+      const float m_new = fmaxf(m_run, mx * c);
+      const float alpha = exp2f_fast(m_run - ((m_new == -INFINITY) ? 0.f : m_new));
+      l_run *= alpha;
+#pragma unroll
+      for (int d = 0; d < DT; ++d)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[d][i] *= alpha;
+      m_run = m_new;
+    }
+    const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
     float psum = 0.f;
     bf16x8 pb[4], pl[4];
 #pragma unroll
@@ -136,27 +153,22 @@ __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
         pb[u * 2 + (i >> 3)][i & 7] = hi;
         if constexpr (HILO) pl[u * 2 + (i >> 3)][i & 7] = to_bf16(p - (float)hi);
       }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-#pragma unroll
-    for (int d = 0; d < DT; ++d)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) acc[d][i] *= alpha;
+    l_run += psum;
 
     // O^T[d][q] += sum_key V[key][d] P[q][key]; the key order inside each
     // 16-key step follows the S^T register layout (see device.hpp).
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      const bf16* vp = Vs + (16 * u + 4 * (G >> 1) + (sl >> 2)) * PITCH + 16 * (G & 1) + 4 * (sl & 3);
+      const bf16* vp = Vs + (16 * u + 4 * (G >> 1) + (sl >> 2)) * PV + 16 * (G & 1) + 4 * (sl & 3);
 #pragma unroll
       for (int d = 0; d < DT; ++d) {
-        const bf16x8 va = cat(lds_read_tr(vp + 32 * d), lds_read_tr(vp + 32 * d + 8 * PITCH));
+        const bf16x8 va = cat(lds_read_tr(vp + 32 * d), lds_read_tr(vp + 32 * d + 8 * PV));
         acc[d] = mfma32(va, pb[u], acc[d]);
         if constexpr (HILO) acc[d] = mfma32(va, pl[u], acc[d]);
       }
     }
 
-    if (have_next) ld.template store<PITCH>(lds + (cur ^ 1) * STAGE, lds + (cur ^ 1) * STAGE + BN * PITCH, tid);
+    if (have_next) ld.template store<PK, PV>(lds + (cur ^ 1) * STAGE, lds + (cur ^ 1) * STAGE + BN * PK, tid);
     __syncthreads();
     cur ^= 1;
     j = jn; t = tn; t1 = t1n; f0 = f0n; f1 = f1n;

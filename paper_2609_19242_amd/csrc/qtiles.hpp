@@ -119,14 +119,17 @@ struct KVTileLoader {
     }
   }
 
-  template <int PITCH>
-  __device__ inline void store(bf16* ks, bf16* vs, int tid) const {
+  // K rows to ks at pitch PK, V rows to vs at pitch PV, and (when k2 is not
+  // null) K a second time to k2 at pitch PK2.
+  template <int PK, int PV, int PK2 = PK>
+  __device__ inline void store(bf16* ks, bf16* vs, int tid, bf16* k2 = nullptr) const {
 #pragma unroll
     for (int n = 0; n < CPT; ++n) {
       const int cidx = tid + n * NT;
       const int row = cidx / CPR, col = cidx % CPR;
-      *(u32x4*)(ks + row * PITCH + col * 8) = pk[n];
-      *(u32x4*)(vs + row * PITCH + col * 8) = pv[n];
+      *(u32x4*)(ks + row * PK + col * 8) = pk[n];
+      *(u32x4*)(vs + row * PV + col * 8) = pv[n];
+      if (k2) *(u32x4*)(k2 + row * PK2 + col * 8) = pk[n];
     }
   }
 };
