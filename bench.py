@@ -187,6 +187,39 @@ def bench_csbp(torch, bd, synth, steps, warmup):
            "merge_roofline": {"bound": "hbm", "kernel": "lse_merge", "achieved": gbs, "peak": PEAK_HBM_GBS,
                               "unit": "GB/s", "frac": gbs / PEAK_HBM_GBS, "bytes_per_launch": merge_bytes,
                               "parts": J, "parts_read": nonempty}}
+
+    # The whole rank operator: the rank's clean-shard queries as well (they attend
+    # causally to the gathered clean shards), one multi-range forward launch for
+    # them and one backward over both query ranges.
+    own = synth.csbp_own_shard(w)
+    S = w.shard_tokens
+    qc, doc = synth.make_csbp_clean_queries(w, device=dev)
+    qrc = bd.Range(bd.CLEAN, own * S, S)
+    oc, dqc = torch.empty_like(qc), torch.empty_like(qc)
+    lc = torch.empty((1, Hq, S), dtype=torch.float32, device=dev)
+    ws2 = torch.empty(bd.attn_bwd_workspace_bytes(p, [qr, qrc]), dtype=torch.uint8, device=dev)
+    pairs2 = bd.visible_pairs(p, [qr, qrc], krs)
+    fl2 = bd.useful_flops(pairs2, Hq, 1, D)
+
+    def rank_step():
+        for j in range(J):
+            bd.attn_partial_fwd(p, qr, q, o_parts[j], l_parts[j], krs[j], ks[j], vs[j])
+        bd.lse_merge(o_parts, l_parts, om, lm)
+        bd.attn_fwd(p, [qrc], [qc], [oc], [lc], krs, ks, vs)
+        bd.attn_bwd(p, [qr, qrc], [q, qc], [om, oc], [lm, lc], [do, doc], [dq, dqc], krs, ks, vs, dks, dvs, ws2)
+
+    for _ in range(warmup):
+        rank_step()
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(steps):
+        rank_step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms2 = e0.elapsed_time(e1) / steps
+    res["rank_operator"] = {"workload": "the same rank plus its 16384 clean-shard queries (shard %d)" % own,
+                            "ms_per_step": ms2, "useful_tflops": fl2["total"] / (ms2 * 1e-3) / 1e12,
+                            "pairs_per_head": pairs2}
     return res
 
 
@@ -271,7 +304,8 @@ def main():
     print(f"[bench] 32k: {main_res['ms_per_step']:.3f} ms/step, {main_res['value']:.1f} useful TFLOP/s", flush=True)
     csbp = None if args.no_csbp else bench_csbp(torch, bd, synth, max(2, args.steps // 2), 1)
     if csbp:
-        print(f"[bench] csbp256k: {csbp['ms_per_step']:.3f} ms/step", flush=True)
+        print(f"[bench] csbp256k: {csbp['ms_per_step']:.3f} ms/step; with clean-shard queries "
+              f"{csbp['rank_operator']['ms_per_step']:.3f} ms/step", flush=True)
     cpu = None if args.no_cpu_baseline else cpu_baseline(bd, synth, args.cpu_budget_s)
     w = main_res["workload"]
     line = {

@@ -152,3 +152,24 @@ def make_csbp_rank(w: Workload, device: str = "cpu", dtype: Optional[torch.dtype
     del kall, vall
     do = normal((1, n, w.heads, w.head_dim), base + 3, dt, device) if need_do else None
     return q, k_local, v_local, k_clean, v_clean, do
+
+
+def csbp_own_shard(w: Workload) -> int:
+    """Index of the clean shard a CSBP rank owns: the one at its corrupted blocks' positions."""
+    assert w.kind == "csbp_rank" and w.local_pos0 % w.shard_tokens == 0
+    return w.local_pos0 // w.shard_tokens
+
+
+def make_csbp_clean_queries(w: Workload, device: str = "cpu", dtype: Optional[torch.dtype] = None,
+                            seed_base: Optional[int] = None):
+    """The rank's clean-shard queries and their upstream gradient: ``q_clean, do_clean``.
+
+    These are the ``shard_tokens`` clean rows the rank owns (positions
+    ``[own * shard_tokens, (own + 1) * shard_tokens)``); seeds are tensors 5 and 6
+    of the workload.
+    """
+    assert w.kind == "csbp_rank"
+    dt = dtype or w.torch_dtype
+    base = 1000 * w.index if seed_base is None else seed_base
+    shape = (1, w.shard_tokens, w.heads, w.head_dim)
+    return normal(shape, base + 5, dt, device), normal(shape, base + 6, dt, device)

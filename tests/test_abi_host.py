@@ -140,3 +140,19 @@ def test_visible_pairs_match_oracle_popcount(L, M, reading):
     want = oracle.count_visible_pairs([(CORRUPTED, 0, L), (CLEAN, 0, L)],
                                       [(CORRUPTED, 0, L), (CLEAN, 3, L - 5), (CLEAN, 0, 3)], M, reading)
     assert got == want
+
+
+def test_visible_pairs_csbp_rank_with_clean_queries():
+    """The rank's clean-shard queries (positions 131072..147455) see clean keys 0..p
+    (clean->clean causal, Sec. 3.2): sum_p (p + 1) on top of the corrupted share."""
+    w = WORKLOADS["csbp256k"]
+    p = bd.make_problem(1, w.L, w.block_size, w.heads, w.kv_heads, w.head_dim, bd.BF16)
+    S = w.shard_tokens
+    own = w.local_pos0 // S
+    qr = [Range(CORRUPTED, w.local_pos0, w.local_tokens), Range(CLEAN, own * S, S)]
+    kr = [Range(CORRUPTED, w.local_pos0, w.local_tokens)] + \
+         [Range(CLEAN, s * S, S) for s in range(w.n_shards)]
+    first, last = own * S, own * S + S - 1
+    clean = (last - first + 1) * (first + 1 + last + 1) // 2
+    assert clean == 2281709568
+    assert bd.visible_pairs(p, qr, kr) == 2281963520 + clean

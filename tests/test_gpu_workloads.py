@@ -207,3 +207,92 @@ def test_workload_csbp256k():
     krow = [n + x for x in kpos]  # rows in the concatenated [local ; clean] key tensor
     assert_close("csbp256k dK last visible clean block", dkc[:, kpos][:, :, kvs], dK[:, krow], BF16)
     assert_close("csbp256k dV last visible clean block", dvc[:, kpos][:, :, kvs], dV[:, krow], BF16)
+
+
+def test_workload_csbp256k_rank_operator():
+    """One CSBP rank with its clean-shard queries too (Alg. 1/2 for one rank).
+
+    The rank owns clean shard 8 (the positions of its corrupted blocks); its
+    clean queries attend causally to all gathered clean keys, i.e. shards 0..8.
+    Forward: corrupted queries by per-range partials + merge, clean queries by
+    one multi-range launch (checked against their own partials + merge);
+    backward: one call over both query ranges and all 17 key ranges.
+    """
+    w = WORKLOADS["csbp256k"]
+    torch.cuda.empty_cache()
+    q, kl, vl, kc, vc, do = synth.make_csbp_rank(w, device=DEV)
+    qc, doc = synth.make_csbp_clean_queries(w, device=DEV)
+    own, S, n, M = synth.csbp_own_shard(w), w.shard_tokens, w.local_tokens, w.block_size
+    qr, krs = csbp_ranges(w)
+    qrc = Range(CLEAN, own * S, S)
+    p = bd.make_problem(1, w.L, w.block_size, w.heads, w.kv_heads, w.head_dim, torch.bfloat16, out_f32=True)
+    ks = [kl.data_ptr()] + shard_views(kc, w)
+    vs = [vl.data_ptr()] + shard_views(vc, w)
+
+    def partials_merged(qrange, qt, rows):
+        o_parts, l_parts = [], []
+        for j, kr in enumerate(krs):
+            o = torch.empty(qt.shape, dtype=F32, device=DEV)
+            lse = torch.empty((1, w.heads, rows), dtype=F32, device=DEV)
+            bd.attn_partial_fwd(p, qrange, qt, o, lse, kr, ks[j], vs[j])
+            o_parts.append(o)
+            l_parts.append(lse)
+        om = torch.empty(qt.shape, dtype=F32, device=DEV)
+        lm = torch.empty((1, w.heads, rows), dtype=F32, device=DEV)
+        bd.lse_merge(o_parts, l_parts, om, lm)
+        return om, lm, l_parts
+
+    om, lm, _ = partials_merged(qr, q, n)
+    oc = torch.empty(qc.shape, dtype=F32, device=DEV)
+    lc = torch.empty((1, w.heads, S), dtype=F32, device=DEV)
+    bd.attn_fwd(p, [qrc], [qc], [oc], [lc], krs, ks, vs)
+    omc, lmc, lpc = partials_merged(qrc, qc, S)
+    torch.cuda.synchronize()
+    # clean queries never see corrupted keys nor shards past their own
+    assert torch.isneginf(lpc[0]).all()
+    for s in range(own + 1, w.n_shards):
+        assert torch.isneginf(lpc[1 + s]).all()
+    assert_close("rank clean fused vs merged O", oc, omc.cpu().double().numpy(), BF16)
+    assert_close("rank clean fused vs merged LSE", lc, lmc.cpu().double().numpy(), BF16)
+
+    dq = torch.empty(q.shape, dtype=F32, device=DEV)
+    dqc = torch.empty(qc.shape, dtype=F32, device=DEV)
+    dkl, dvl = (torch.empty(t.shape, dtype=F32, device=DEV) for t in (kl, vl))
+    dkc, dvc = (torch.empty(t.shape, dtype=F32, device=DEV) for t in (kc, vc))
+    ws = torch.empty(bd.attn_bwd_workspace_bytes(p, [qr, qrc]), dtype=torch.uint8, device=DEV)
+    bd.attn_bwd(p, [qr, qrc], [q, qc], [om, oc], [lm, lc], [do, doc], [dq, dqc], krs, ks, vs,
+                [dkl.data_ptr()] + shard_views(dkc, w), [dvl.data_ptr()] + shard_views(dvc, w), ws)
+    torch.cuda.synchronize()
+    dv_identity(torch.cat([dvl, dvc], dim=1), torch.cat([do, doc], dim=1), w.heads // w.kv_heads, "csbp256k rank")
+    # clean keys past the rank's own shard are seen by nobody on this rank
+    assert (dkc[:, (own + 1) * S:] == 0).all() and (dvc[:, (own + 1) * S:] == 0).all()
+
+    kvs = [0, w.kv_heads - 1]
+    hs = kv_group_heads(w.heads, w.kv_heads, kvs)
+    qcat = torch.cat([q, qc], dim=1)[:, :, hs].cpu()
+    docat = torch.cat([do, doc], dim=1)[:, :, hs].cpu()
+    kall = torch.cat([kl, kc], dim=1)[:, :, kvs].cpu()
+    vall = torch.cat([vl, vc], dim=1)[:, :, kvs].cpu()
+    qranges = [(CORRUPTED, w.local_pos0, n), (CLEAN, own * S, S)]
+    kranges = [(r.stream, r.pos0, r.len) for r in krs]
+
+    def single(rows):
+        return [(CORRUPTED, w.local_pos0 + i, 1) if i < n else (CLEAN, own * S + i - n, 1) for i in rows]
+
+    rng = np.random.default_rng(5)
+    crow = sorted(set([0, 1, M - 1, M, S // 2, S - M, S - 1] + rng.choice(S, 12, replace=False).tolist()))
+    rows = [n + i for i in crow]
+    O, LSE = oracle.fwd(qcat, kall, vall, qranges, kranges, M, q_rows=rows)
+    assert_close("rank clean O rows", oc[:, crow][:, :, hs], O, BF16)
+    assert_close("rank clean LSE rows", lc[:, hs][:, :, crow], LSE, BF16)
+    dQ, _, _ = oracle.bwd(qcat[:, rows], kall, vall, O, LSE, docat[:, rows], single(rows), kranges, M)
+    assert_close("rank clean dQ rows", dqc[:, crow][:, :, hs], dQ, BF16)
+    # the last two clean key blocks of the own shard: seen by the last two blocks of
+    # clean queries and (for the earlier block) the last corrupted block
+    qrows = list(range(n - M, n)) + [n + i for i in range(S - 2 * M, S)]
+    Oq, Lq = oracle.fwd(qcat, kall, vall, qranges, kranges, M, q_rows=qrows)
+    _, dK, dV = oracle.bwd(qcat[:, qrows], kall, vall, Oq, Lq, docat[:, qrows], single(qrows), kranges, M)
+    kpos = list(range((own + 1) * S - 2 * M, (own + 1) * S))
+    krow = [n + x for x in kpos]
+    assert_close("rank own-shard tail dK", dkc[:, kpos][:, :, kvs], dK[:, krow], BF16)
+    assert_close("rank own-shard tail dV", dvc[:, kpos][:, :, kvs], dV[:, krow], BF16)
