@@ -273,6 +273,8 @@ def main():
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-csbp", action="store_true")
+    ap.add_argument("--csbp-only", action="store_true",
+                    help="run only the 256K CSBP leg and print its result (for per-workload kernel profiles)")
     ap.add_argument("--pmc-pass", action="store_true",
                     help="one 32K fwd+bwd step and a plain 1 GiB device copy, for rocprofv3 counter runs")
     args = ap.parse_args()
@@ -299,6 +301,10 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         print("[bench] pmc pass done", flush=True)
+        return
+    if args.csbp_only:
+        res = bench_csbp(torch, bd, synth, args.steps, args.warmup)
+        print(json.dumps({"csbp256k": res}), flush=True)
         return
     main_res = bench_32k(torch, bd, synth, args.steps, args.warmup)
     print(f"[bench] 32k: {main_res['ms_per_step']:.3f} ms/step, {main_res['value']:.1f} useful TFLOP/s", flush=True)
