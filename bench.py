@@ -48,10 +48,13 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_32k.json")
 
 
 def kernel_source_hash(kernel):
+    """Hash of a kernel's sources and of their per-source compile options."""
+    from paper_2609_19242_amd import build
     h = hashlib.sha256()
     for f in KERNEL_SOURCES.get(kernel, []):
         with open(os.path.join(ROOT, "paper_2609_19242_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
+        h.update(" ".join(build.EXTRA_FLAGS.get(f, [])).encode())
     return h.hexdigest()[:16]
 
 

@@ -20,10 +20,12 @@ BUILD_DIR = os.path.join(HERE, "_build")
 SOURCES = ["api.cpp", "fwd_bf16.hip", "fwd_f32.hip", "merge.hip", "bwd_pre.hip", "bwd_bf16.hip", "bwd_dq.hip", "bwd_f32.hip"]
 ARCH = os.environ.get("BDLM_OFFLOAD_ARCH", "gfx950")
 # Per-source code-generation options.  The dK/dV kernel runs one wave per SIMD,
-# so nothing hides its LDS latency but the wave's own instruction order; the
-# iterative ILP scheduler keeps more LDS reads in flight there (measured 44.4 ->
-# 42.9 ms at L=32768; it is slower for the two-waves-per-SIMD kernels).
-EXTRA_FLAGS = {"bwd_bf16.hip": ["-mllvm", "-amdgpu-sched-strategy=iterative-ilp"]}
+# so its speed is its own instruction stream: the iterative ILP scheduler keeps
+# more LDS reads in flight, and VGPR-form MFMAs stop the register allocator from
+# sharing AGPRs between the per-step S/dP tiles and the dK/dV accumulators
+# (about 190 -> 70 register-file copies per step).  Measured at L=32768:
+# 44.4 -> 42.9 -> 38.9 ms; both are slower for the two-waves-per-SIMD kernels.
+EXTRA_FLAGS = {"bwd_bf16.hip": ["-mllvm", "-amdgpu-sched-strategy=iterative-ilp", "-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
 def hipcc() -> str:
