@@ -36,29 +36,28 @@ struct BwdStage {
 };
 
 // Global -> LDS copy plan of one step.  Each tensor (Q, dO) of a stage is
-// NH * 32 rows of PITCH / 8 16-byte slots; a copy instruction fills 64
-// consecutive slots (one per lane) and the pad slots get an out-of-range
-// offset.  Tensor instructions g = 0 .. 2 TI - 1 go to wave g % 4; waves 2
-// and 3 copy the LSE*log2(e) and D rows (one dword instruction each).  NMIN is
-// the smallest per-wave instruction count of a step: waiting
-// for vmcnt <= NMIN after issuing the next step leaves only that step's copies
-// in flight.
+// NH * 32 rows of PITCH / 8 16-byte slots, TI copy instructions of 64
+// consecutive slots (one per lane; the pad slots get an out-of-range offset).
+// Waves 0 and 1 copy Q, waves 2 and 3 copy dO, each wave one half of the
+// tensor's instructions (the first half to the even wave), so a wave's copies
+// need no per-instruction choice of tensor; waves 2 and 3 also copy the
+// LSE*log2(e) and D rows (one dword instruction each).  NMIN is the smallest
+// per-wave instruction count of a step: waiting for vmcnt <= NMIN after
+// issuing the next step leaves only that step's copies in flight.
 template <int D, int NH>
 struct CopyPlan {
   static constexpr int SLOTS = BwdStage<D, NH>::PITCH / 8;
   static constexpr int TI = NH * 32 * SLOTS / 64;
-  static constexpr int IPW = (2 * TI + 3) / 4;
-  static constexpr int count(int w) { return (2 * TI - w + 3) / 4 + (w >= 2 ? 1 : 0); }
-  static constexpr int NMIN = count(0) < count(1) ? (count(0) < count(2) ? (count(0) < count(3) ? count(0) : count(3))
-                                                                         : (count(2) < count(3) ? count(2) : count(3)))
-                                                  : (count(1) < count(2) ? (count(1) < count(3) ? count(1) : count(3))
-                                                                         : (count(2) < count(3) ? count(2) : count(3)));
+  static constexpr int IPW = (TI + 1) / 2;  // instructions of the even wave; the odd wave has TI - IPW
+  static constexpr int NMIN = TI - IPW;
   static_assert((NH * 32 * SLOTS) % 64 == 0, "whole copy instructions per tensor");
 };
 
 constexpr uint32_t kOutOfRange = 0x7fff0000u;
 
-template <int D, bool HILO, int NH>
+// NQ: query-range slots the walk considers (2 when the call has at most two
+// query ranges, else kMaxQ); fewer slots keep the walk state in fewer registers.
+template <int D, bool HILO, int NH, int NQ>
 __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
   constexpr int BN = kBwdKeysBf16, BM = 32, KS = D / 16, DT = D / 32;
   using Stage = BwdStage<D, NH>;
@@ -131,17 +130,30 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
   // every pair of query heads.  Visible query rows extend to the end of a range
   // for every key tile, so all workgroups resident on an XCD start on the same
   // rows and stay close together: their Q/dO reads are shared in L2.
-  // Per range: steps [s0, s1), fully visible steps [f0, f1), and the queries
-  // [qa, qa + qw) of the range that see this lane's key.  Four named slots
-  // (not an array) so that every field stays in registers.
+  // Per range: steps [s0, s1), fully visible steps [f0, f1), the queries
+  // [qa, qa + qw) of the range that see this lane's key, and the copy bases of
+  // this wave (its tensor at the first row and first head of the group; for
+  // waves 2 and 3 the LSE*log2(e) or D row of that head, and the bytes from
+  // there to the end of the array).  Named slots (not an array) so that every
+  // field stays in registers.
   struct Span {
-    int s0, s1, f0, f1, pos0, qa, qw;
+    int s0, s1, f0, f1, pos0, qa, qw, len;
+    const bf16* tb;
+    const float* lb;
+    uint32_t lrec;
   };
+  static_assert(NQ == 2 || NQ == kMaxQ, "query-range slots");
   auto make_span = [&](int q) -> Span {
-    Span sp{0, 0, 0, 0, 0, 0, 0};
-    if (q >= a.n_q) return sp;
+    Span sp{0, 0, 0, 0, 0, 0, 0, 0, nullptr, nullptr, 0u};
+    if (q >= NQ || q >= a.n_q) return sp;
     const QRangeArg& qr = a.qr[q];
     sp.pos0 = qr.pos0;
+    sp.len = qr.len;
+    const int h0 = kvh * a.group;
+    sp.tb = (const bf16*)(w < 2 ? qr.q : qr.dO) + ((int64_t)b * qr.bstride * H + h0) * D;
+    const int64_t lrow = ((int64_t)b * H + h0) * qr.len;
+    sp.lb = (w == 2 ? qr.l2 : qr.delta) + lrow;
+    sp.lrec = (uint32_t)(((int64_t)a.batch * H * qr.len - lrow) * 4);
     int lo0, hi0, lo1, hi1;
     query_interval(qr.stream, kr.stream, kpos_first, a.M, a.intra, lo0, hi0);
     query_interval(qr.stream, kr.stream, kpos_last, a.M, a.intra, lo1, hi1);
@@ -166,7 +178,10 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
   static_assert(kMaxQ == 4, "four range slots");
   const Span R0 = make_span(0), R1 = make_span(1), R2 = make_span(2), R3 = make_span(3);
   // Select by value (a select of member addresses would force the spans into memory).
-  auto sel4 = [](int q, int v0, int v1, int v2, int v3) { return q == 0 ? v0 : q == 1 ? v1 : q == 2 ? v2 : v3; };
+  auto sel4 = [](int q, auto v0, auto v1, auto v2, auto v3) {
+    if constexpr (NQ == 2) return q ? v1 : v0;
+    else return q == 0 ? v0 : q == 1 ? v1 : q == 2 ? v2 : v3;
+  };
 #define BDLM_PICK(f, q) sel4((q), R0.f, R1.f, R2.f, R3.f)
   auto active = [](const Span& sp, int s) { return sp.s0 <= s && s < sp.s1; };
   // First range after q that is active at step s (kMaxQ if none).
@@ -201,44 +216,43 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
     return c;
   };
 
-  // ---- copy plan: per-lane global offsets of this wave's tensor instructions
-  // (constant over the walk; the step moves the resource base).
+  // ---- copy plan: per-lane global byte offsets of this wave's instructions
+  // inside one step's NH heads x 32 rows (constant over the walk; the step
+  // moves the resource base).  Instruction i of the wave is instruction
+  // (w & 1) * IPW + i of its tensor.
+  const int wodd = w & 1;
   uint32_t voff[Plan::IPW];
 #pragma unroll
   for (int i = 0; i < Plan::IPW; ++i) {
-    const int g = 4 * i + w;
-    const int slot = (g % Plan::TI) * 64 + lane;
+    const int g = wodd * Plan::IPW + i;
+    const int slot = g * 64 + lane;
     const int row = slot / Plan::SLOTS, ch = slot % Plan::SLOTS;
     const int j = row / BM, rr = row % BM;
-    voff[i] = (g < 2 * Plan::TI && ch < D / 8) ? (uint32_t)(((rr * H + j) * D + ch * 8) * 2) : kOutOfRange;
+    voff[i] = (g < Plan::TI && ch < D / 8) ? (uint32_t)(((rr * H + j) * D + ch * 8) * 2) : kOutOfRange;
   }
-  // Issue the copies of step c into stage S (an empty copy when c is past the end).
+  // Issue the copies of step c into stage S (empty copies when c is past the end).
   auto copy_step = [&](Stage& S, const Cursor c) __attribute__((always_inline)) {
     const bool live = c.s >= 0;
-    const QRangeArg& qr = a.qr[live ? c.q : 0];
-    const int h0 = kvh * a.group + c.hp * NH;
+    const int q = live ? c.q : 0;
     const int row0 = c.s * BM;
-    const int nrows = live ? imin(BM, qr.len - row0) : 0;
-    const int64_t qoff = (((int64_t)b * qr.bstride + row0) * H + h0) * D;
-    const uint32_t qbytes = live ? (uint32_t)(((int64_t)(nrows - 1) * H + NH) * D * 2) : 0u;
-    const auto rq = make_rsrc((const bf16*)qr.q + (live ? qoff : 0), qbytes);
-    const auto rdo = make_rsrc((const bf16*)qr.dO + (live ? qoff : 0), qbytes);
+    const int len = BDLM_PICK(len, q);
+    const int nrows = live ? imin(BM, len - row0) : 0;
+    const int hoff = c.hp * NH;
+    const uint32_t bytes = live ? (uint32_t)(((int64_t)(nrows - 1) * H + NH) * D * 2) : 0u;
+    const auto rt = make_rsrc(BDLM_PICK(tb, q) + ((int64_t)row0 * H + hoff) * D, bytes);
+    bf16* dst = (w < 2 ? S.q : S.dO) + wodd * Plan::IPW * 512;
 #pragma unroll
-    for (int i = 0; i < Plan::IPW; ++i) {
-      const int g = 4 * i + w;
-      if (g < Plan::TI) buf_to_lds<16>(rq, S.q + g * 512, voff[i], 0);
-      else if (g < 2 * Plan::TI) buf_to_lds<16>(rdo, S.dO + (g - Plan::TI) * 512, voff[i], 0);
-    }
+    for (int i = 0; i < Plan::IPW; ++i)
+      if (Plan::TI % 2 == 0 || i + 1 < Plan::IPW || wodd == 0) buf_to_lds<16>(rt, dst + i * 512, voff[i], 0);
     if (w >= 2) {
       // LSE*log2(e) (wave 2) or D (wave 3) of the NH heads' rows, [head][row]
       // floats.  Each resource ends with its array, so rows past the end of the
       // last head read zeros; other rows past the range end read finite values
       // of the next head (those rows are always masked).
-      const int64_t loff = ((int64_t)b * H + h0) * qr.len + row0;
-      const int64_t total = (int64_t)a.batch * H * qr.len;
-      const uint32_t lbytes = live ? (uint32_t)((total - loff) * 4) : 0u;
-      const auto rl = make_rsrc((w == 2 ? qr.l2 : qr.delta) + (live ? loff : 0), lbytes);
-      const uint32_t vo = NH == 2 ? (uint32_t)(((lane >> 5) * qr.len + (lane & 31)) * 4) : (uint32_t)(lane * 4);
+      const int64_t loff = (int64_t)hoff * len + row0;
+      const uint32_t lbytes = live ? BDLM_PICK(lrec, q) - (uint32_t)(loff * 4) : 0u;
+      const auto rl = make_rsrc(BDLM_PICK(lb, q) + loff, lbytes);
+      const uint32_t vo = NH == 2 ? (uint32_t)(((lane >> 5) * len + (lane & 31)) * 4) : (uint32_t)(lane * 4);
       buf_to_lds<4>(rl, w == 2 ? S.l2 : S.dl, vo, 0);
     }
   };
@@ -389,23 +403,29 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
 
 }  // namespace
 
-template <int D, bool HILO>
+template <int D, bool HILO, int NQ>
 void launch_nh(const AttnArgs& a, int n, hipStream_t s) {
   if (a.group % 2 == 0)
-    hipLaunchKernelGGL((bwd_bf16_kernel<D, HILO, 2>), dim3(n), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((bwd_bf16_kernel<D, HILO, 2, NQ>), dim3(n), dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL((bwd_bf16_kernel<D, HILO, 1>), dim3(n), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((bwd_bf16_kernel<D, HILO, 1, NQ>), dim3(n), dim3(256), 0, s, a);
+}
+
+template <int D, bool HILO>
+void launch_nq(const AttnArgs& a, int n, hipStream_t s) {
+  if (a.n_q <= 2) launch_nh<D, HILO, 2>(a, n, s);
+  else launch_nh<D, HILO, kMaxQ>(a, n, s);
 }
 
 hipError_t launch_bwd_bf16(const AttnArgs& a, int head_dim, hipStream_t s) {
   const int n = a.total_tiles * a.kv_heads * a.batch;
   if (n == 0) return hipSuccess;
   if (head_dim == 128) {
-    if (a.hilo) launch_nh<128, true>(a, n, s);
-    else launch_nh<128, false>(a, n, s);
+    if (a.hilo) launch_nq<128, true>(a, n, s);
+    else launch_nq<128, false>(a, n, s);
   } else {
-    if (a.hilo) launch_nh<64, true>(a, n, s);
-    else launch_nh<64, false>(a, n, s);
+    if (a.hilo) launch_nq<64, true>(a, n, s);
+    else launch_nq<64, false>(a, n, s);
   }
   return hipGetLastError();
 }

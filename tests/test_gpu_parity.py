@@ -218,3 +218,50 @@ def test_empty_rows_partial():
     O, LSE = oracle.fwd(q[:, :L], k[:, L:], v[:, L:], [(CORRUPTED, 0, L)], [(CLEAN, 0, L)], M)
     assert_close("empty-rows O", o, O, torch.bfloat16)
     assert_close("empty-rows LSE", lse, LSE, torch.bfloat16)
+
+
+# ------------------------------------------- more than two query ranges
+@pytest.mark.parametrize("split", ["q3-k3", "q4-k4"])
+@pytest.mark.parametrize("heads", [(4, 2, 128), (3, 1, 64)], ids=["H4x2-d128", "H3x1-d64"])
+def test_multi_range_fwd_bwd(split, heads):
+    """The joint problem cut into three or four query ranges and as many key
+    ranges (uneven cuts, each range its own tensor), forward and backward in one
+    call each, against the oracle over the same ranges."""
+    Hq, Hkv, D = heads
+    L, M = 300, 12
+    q, k, v, do = joint_inputs(L, Hq, Hkv, D, torch.bfloat16, seed=41 + D)
+    cuts = {"q3-k3": ([(CORRUPTED, 0, 140), (CORRUPTED, 140, 160), (CLEAN, 0, 300)],
+                      [(CLEAN, 0, 90), (CLEAN, 90, 210), (CORRUPTED, 0, 300)]),
+            "q4-k4": ([(CLEAN, 170, 130), (CORRUPTED, 0, 97), (CLEAN, 0, 170), (CORRUPTED, 97, 203)],
+                      [(CORRUPTED, 150, 150), (CLEAN, 0, 300), (CORRUPTED, 0, 33), (CORRUPTED, 33, 117)])}[split]
+    qrs, krs = cuts
+
+    def rows(t, rs):  # joint tensors hold corrupted rows [0, L) then clean rows [L, 2L)
+        return [t[:, (L if s == CLEAN else 0) + p0:(L if s == CLEAN else 0) + p0 + n].contiguous() for s, p0, n in rs]
+
+    qs, dos = rows(q, qrs), rows(do, qrs)
+    ks, vs = rows(k, krs), rows(v, krs)
+    p = bd.make_problem(1, L, M, Hq, Hkv, D, torch.bfloat16, out_f32=True)
+    QR = [Range(*r) for r in qrs]
+    KR = [Range(*r) for r in krs]
+    qd, dod = [t.to(DEV) for t in qs], [t.to(DEV) for t in dos]
+    kd, vd = [t.to(DEV) for t in ks], [t.to(DEV) for t in vs]
+    od = [torch.empty(t.shape, dtype=torch.float32, device=DEV) for t in qd]
+    ld = [torch.empty((1, Hq, t.shape[1]), dtype=torch.float32, device=DEV) for t in qd]
+    bd.attn_fwd(p, QR, qd, od, ld, KR, kd, vd)
+    dqd = [torch.empty(t.shape, dtype=torch.float32, device=DEV) for t in qd]
+    dkd = [torch.empty(t.shape, dtype=torch.float32, device=DEV) for t in kd]
+    dvd = [torch.empty(t.shape, dtype=torch.float32, device=DEV) for t in vd]
+    ws = torch.empty(bd.attn_bwd_workspace_bytes(p, QR), dtype=torch.uint8, device=DEV)
+    bd.attn_bwd(p, QR, qd, od, ld, dod, dqd, KR, kd, vd, dkd, dvd, ws)
+    torch.cuda.synchronize()
+
+    qall, doall = torch.cat(qs, dim=1), torch.cat(dos, dim=1)
+    kall, vall = torch.cat(ks, dim=1), torch.cat(vs, dim=1)
+    O, LSE = oracle.fwd(qall, kall, vall, qrs, krs, M)
+    dQ, dK, dV = oracle.bwd(qall, kall, vall, O, LSE, doall, qrs, krs, M)
+    assert_close(f"{split} O", torch.cat([t.cpu() for t in od], dim=1), O, torch.bfloat16)
+    assert_close(f"{split} LSE", torch.cat([t.cpu() for t in ld], dim=2), LSE, torch.bfloat16)
+    assert_close(f"{split} dQ", torch.cat([t.cpu() for t in dqd], dim=1), dQ, torch.bfloat16)
+    assert_close(f"{split} dK", torch.cat([t.cpu() for t in dkd], dim=1), dK, torch.bfloat16)
+    assert_close(f"{split} dV", torch.cat([t.cpu() for t in dvd], dim=1), dV, torch.bfloat16)
