@@ -28,32 +28,60 @@ namespace {
 
 template <int D, int NH>
 struct BwdStage {
-  static constexpr int PITCH = D + 16;  // LDS row pitch in elements (two 16-byte pad slots)
-  bf16 q[NH * 32 * PITCH];
-  bf16 dO[NH * 32 * PITCH];
+  // Rows of D elements, no padding; the 16-byte chunks of a row are permuted
+  // by chunk_swz (below) so that neither access pattern has bank conflicts.
+  bf16 q[NH * 32 * D];
+  bf16 dO[NH * 32 * D];
   float l2[64];  // [head][row]: LSE * log2(e)  (64 floats: one copy instruction)
   float dl[64];  // [head][row]: D
 };
 
+// Q and dO rows in a stage are unpadded; logical 16-byte chunk c of row r sits
+// in physical chunk c ^ chunk_swz<D>(r).  The two read patterns of a step are
+// 64-lane ds_read_b128 row reads (16 lanes per LDS cycle: 16 rows, one chunk
+// each) and ds_read_b64_tr_b16 transpose reads (32 lanes per cycle: 4
+// consecutive rows, 64 bytes each).  With 256-byte rows (D = 128) the 16 rows
+// of a row read land in 16 distinct chunk columns and the 4 rows of a
+// transpose read in 4 disjoint quarter-rows, so both are conflict-free (64
+// banks x 4 bytes); for D = 64 (128-byte rows, two rows per bank period) the
+// same holds with the second function.  Padding alone cannot do both: 272-byte
+// rows are 4-way on transpose reads, 320-byte rows 4-way on row reads, and
+// 288-byte rows 2-way on each.  The function depends on r mod 16 only.
+template <int D>
+__host__ __device__ constexpr int chunk_swz(int r) {
+  return D == 128 ? (((r & 3) << 2) | ((r >> 2) & 3)) : ((((r >> 1) & 1) << 2) | ((r >> 2) & 3));
+}
+
 // Global -> LDS copy plan of one step.  Each tensor (Q, dO) of a stage is
-// NH * 32 rows of PITCH / 8 16-byte slots, TI copy instructions of 64
-// consecutive slots (one per lane; the pad slots get an out-of-range offset).
-// Waves 0 and 1 copy Q, waves 2 and 3 copy dO, each wave one half of the
-// tensor's instructions (the first half to the even wave), so a wave's copies
-// need no per-instruction choice of tensor; waves 2 and 3 also copy the
+// NH * 32 rows of D / 8 16-byte chunks, TI copy instructions of 64
+// consecutive slots (one per lane; a lane fetches the logical chunk that
+// belongs in its physical slot).  Waves 0 and 1 copy Q, waves 2 and 3 copy
+// dO, each wave one half of the tensor's instructions, so a wave's copies need
+// no per-instruction choice of tensor; waves 2 and 3 also copy the
 // LSE*log2(e) and D rows (one dword instruction each).  NMIN is the smallest
 // per-wave instruction count of a step: waiting for vmcnt <= NMIN after
 // issuing the next step leaves only that step's copies in flight.
 template <int D, int NH>
 struct CopyPlan {
-  static constexpr int SLOTS = BwdStage<D, NH>::PITCH / 8;
+  static constexpr int SLOTS = D / 8;
   static constexpr int TI = NH * 32 * SLOTS / 64;
-  static constexpr int IPW = (TI + 1) / 2;  // instructions of the even wave; the odd wave has TI - IPW
-  static constexpr int NMIN = TI - IPW;
-  static_assert((NH * 32 * SLOTS) % 64 == 0, "whole copy instructions per tensor");
+  static constexpr int IPW = TI / 2;
+  static constexpr int NMIN = IPW;
+  static_assert(TI % 2 == 0, "whole copy instructions per wave");
 };
 
-constexpr uint32_t kOutOfRange = 0x7fff0000u;
+// 32-bit LDS addresses: stage bases are 256-byte aligned, so XOR-ing chunk
+// bits into a row address never carries into the row bits.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p;
+}
+__device__ __forceinline__ bf16x8 lds_load16(uint32_t a) {
+  return *(__attribute__((address_space(3))) const bf16x8*)(uintptr_t)a;
+}
+__device__ __forceinline__ bf16x4 lds_read_tr_at(uint32_t a) {
+  return __builtin_bit_cast(bf16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                                        (__attribute__((address_space(3))) short4_t*)(uintptr_t)a));
+}
 
 // NQ: query-range slots the walk considers (2 when the call has at most two
 // query ranges, else kMaxQ); fewer slots keep the walk state in fewer registers.
@@ -62,9 +90,10 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
   constexpr int BN = kBwdKeysBf16, BM = 32, KS = D / 16, DT = D / 32;
   using Stage = BwdStage<D, NH>;
   using Plan = CopyPlan<D, NH>;
-  constexpr int PITCH = Stage::PITCH;
+  constexpr uint32_t RB = D * 2, HB = BM * RB, TB = NH * HB;  // row, head and tensor bytes in a stage
   static_assert(BN == 128, "tile shape");
-  __shared__ __attribute__((aligned(16))) Stage stages[3];
+  static_assert(sizeof(Stage) % 256 == 0, "stage bases stay 256-byte aligned");
+  __shared__ __attribute__((aligned(256))) Stage stages[3];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -111,6 +140,12 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
       kf[s] = __builtin_bit_cast(bf16x8, buf_load16(rk, off + 32 * s));
       vf[s] = __builtin_bit_cast(bf16x8, buf_load16(rv, off + 32 * s));
     }
+    // Keep the K/V operands in AGPRs: MFMAs read their A/B operands from AGPRs
+    // directly, while the VGPRs go to the accumulators and the per-step tiles.
+    // Left to itself the allocator spills them to AGPRs and copies each one
+    // back before every use (64 register-file copies per step).
+#pragma unroll
+    for (int s = 0; s < KS; ++s) asm volatile("" : "+a"(kf[s]), "+a"(vf[s]));
   }
 
   f32x16 dka[DT], dva[DT];
@@ -224,11 +259,10 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
   uint32_t voff[Plan::IPW];
 #pragma unroll
   for (int i = 0; i < Plan::IPW; ++i) {
-    const int g = wodd * Plan::IPW + i;
-    const int slot = g * 64 + lane;
-    const int row = slot / Plan::SLOTS, ch = slot % Plan::SLOTS;
+    const int slot = (wodd * Plan::IPW + i) * 64 + lane;
+    const int row = slot / Plan::SLOTS, ch = (slot % Plan::SLOTS) ^ chunk_swz<D>(row);
     const int j = row / BM, rr = row % BM;
-    voff[i] = (g < Plan::TI && ch < D / 8) ? (uint32_t)(((rr * H + j) * D + ch * 8) * 2) : kOutOfRange;
+    voff[i] = (uint32_t)(((rr * H + j) * D + ch * 8) * 2);
   }
   // Issue the copies of step c into stage S (empty copies when c is past the end).
   auto copy_step = [&](Stage& S, const Cursor c) __attribute__((always_inline)) {
@@ -242,8 +276,7 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
     const auto rt = make_rsrc(BDLM_PICK(tb, q) + ((int64_t)row0 * H + hoff) * D, bytes);
     bf16* dst = (w < 2 ? S.q : S.dO) + wodd * Plan::IPW * 512;
 #pragma unroll
-    for (int i = 0; i < Plan::IPW; ++i)
-      if (Plan::TI % 2 == 0 || i + 1 < Plan::IPW || wodd == 0) buf_to_lds<16>(rt, dst + i * 512, voff[i], 0);
+    for (int i = 0; i < Plan::IPW; ++i) buf_to_lds<16>(rt, dst + i * 512, voff[i], 0);
     if (w >= 2) {
       // LSE*log2(e) (wave 2) or D (wave 3) of the NH heads' rows, [head][row]
       // floats.  Each resource ends with its array, so rows past the end of the
@@ -258,6 +291,11 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
   };
 
   const float c = a.scale_log2;
+  // Per-lane parts of the swizzled LDS read addresses (see chunk_swz).
+  const uint32_t yrow = l32 * RB + ((half ^ chunk_swz<D>(l32)) * 16);
+  const int r0 = 4 * (G >> 1) + (sl >> 2), ch0 = 2 * (G & 1) + ((sl >> 1) & 1);
+  const uint32_t ytr0 = r0 * RB + ((ch0 ^ chunk_swz<D>(r0)) * 16) + 8 * (sl & 1);
+  const uint32_t ytr1 = (r0 + 8) * RB + ((ch0 ^ chunk_swz<D>(r0 + 8)) * 16) + 8 * (sl & 1);
   // One step of the walk on stage S: S = Q K^T, dP = dO V^T, P, dS, then
   // dV^T += dO^T P, dK^T += Q^T dS for every head of the pair.
   auto compute_step = [&](const Stage& S, const Cursor cu) __attribute__((always_inline)) {
@@ -265,11 +303,12 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
     const int mbase = BDLM_PICK(pos0, cu.q) + cu.s * BM + 4 * half - BDLM_PICK(qa, cu.q);
     const int lane_qw = BDLM_PICK(qw, cu.q);
 
+    // Row reads: lane (half, l32) reads logical chunk 2k + half of row l32,
+    // i.e. zr ^ 32k; heads and the dO tensor are immediate offsets.
+    const uint32_t zr = lds_addr(&S) + yrow;
     f32x16 sacc[NH], dpacc[NH];
 #pragma unroll
     for (int j = 0; j < NH; ++j) {
-      const bf16* qs = S.q + j * BM * PITCH;
-      const bf16* dos = S.dO + j * BM * PITCH;
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         sacc[j][i] = 0.f;
@@ -277,8 +316,9 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
       }
 #pragma unroll
       for (int k = 0; k < KS; ++k) {
-        sacc[j] = mfma32(*(const bf16x8*)(qs + l32 * PITCH + 8 * half + 16 * k), kf[k], sacc[j]);
-        dpacc[j] = mfma32(*(const bf16x8*)(dos + l32 * PITCH + 8 * half + 16 * k), vf[k], dpacc[j]);
+        const uint32_t a = (zr ^ (32u * k)) + j * HB;
+        sacc[j] = mfma32(lds_load16(a), kf[k], sacc[j]);
+        dpacc[j] = mfma32(lds_load16(a + TB), vf[k], dpacc[j]);
       }
     }
 
@@ -314,17 +354,19 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
 
     // dV^T += dO^T P and dK^T += Q^T dS (queries are the contraction index),
     // one head and one 16-query half at a time with its transposed fragments.
+    // Transpose reads: rows 16u + R0 (zt0) and 16u + R0 + 8 (zt1), logical
+    // 8-byte piece 8d + 4 (G & 1) + (sl & 3) of the row, i.e. zt ^ 64d.
+    const uint32_t zt0 = lds_addr(&S) + ytr0, zt1 = lds_addr(&S) + ytr1;
 #pragma unroll
     for (int j = 0; j < NH; ++j) {
-      const bf16* qs = S.q + j * BM * PITCH;
-      const bf16* dos = S.dO + j * BM * PITCH;
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
-        const int off = (16 * u + 4 * (G >> 1) + (sl >> 2)) * PITCH + 16 * (G & 1) + 4 * (sl & 3);
 #pragma unroll
         for (int d = 0; d < DT; ++d) {
-          const bf16x8 doT = cat(lds_read_tr(dos + off + 32 * d), lds_read_tr(dos + off + 32 * d + 8 * PITCH));
-          const bf16x8 qT = cat(lds_read_tr(qs + off + 32 * d), lds_read_tr(qs + off + 32 * d + 8 * PITCH));
+          const uint32_t a0 = (zt0 ^ (64u * d)) + j * HB + u * 16 * RB;
+          const uint32_t a1 = (zt1 ^ (64u * d)) + j * HB + u * 16 * RB;
+          const bf16x8 doT = cat(lds_read_tr_at(a0 + TB), lds_read_tr_at(a1 + TB));
+          const bf16x8 qT = cat(lds_read_tr_at(a0), lds_read_tr_at(a1));
           dva[d] = mfma32(doT, pb[j][u], dva[d]);
           if constexpr (HILO) dva[d] = mfma32(doT, pl[j][u], dva[d]);
           dka[d] = mfma32(qT, dsb[j][u], dka[d]);
