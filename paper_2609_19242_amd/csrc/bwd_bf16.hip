@@ -29,28 +29,12 @@ namespace {
 template <int D, int NH>
 struct BwdStage {
   // Rows of D elements, no padding; the 16-byte chunks of a row are permuted
-  // by chunk_swz (below) so that neither access pattern has bank conflicts.
+  // by chunk_swz (device.hpp) so that neither access pattern has bank conflicts.
   bf16 q[NH * 32 * D];
   bf16 dO[NH * 32 * D];
   float l2[64];  // [head][row]: LSE * log2(e)  (64 floats: one copy instruction)
   float dl[64];  // [head][row]: D
 };
-
-// Q and dO rows in a stage are unpadded; logical 16-byte chunk c of row r sits
-// in physical chunk c ^ chunk_swz<D>(r).  The two read patterns of a step are
-// 64-lane ds_read_b128 row reads (16 lanes per LDS cycle: 16 rows, one chunk
-// each) and ds_read_b64_tr_b16 transpose reads (32 lanes per cycle: 4
-// consecutive rows, 64 bytes each).  With 256-byte rows (D = 128) the 16 rows
-// of a row read land in 16 distinct chunk columns and the 4 rows of a
-// transpose read in 4 disjoint quarter-rows, so both are conflict-free (64
-// banks x 4 bytes); for D = 64 (128-byte rows, two rows per bank period) the
-// same holds with the second function.  Padding alone cannot do both: 272-byte
-// rows are 4-way on transpose reads, 320-byte rows 4-way on row reads, and
-// 288-byte rows 2-way on each.  The function depends on r mod 16 only.
-template <int D>
-__host__ __device__ constexpr int chunk_swz(int r) {
-  return D == 128 ? (((r & 3) << 2) | ((r >> 2) & 3)) : ((((r >> 1) & 1) << 2) | ((r >> 2) & 3));
-}
 
 // Global -> LDS copy plan of one step.  Each tensor (Q, dO) of a stage is
 // NH * 32 rows of D / 8 16-byte chunks, TI copy instructions of 64
@@ -69,19 +53,6 @@ struct CopyPlan {
   static constexpr int NMIN = IPW;
   static_assert(TI % 2 == 0, "whole copy instructions per wave");
 };
-
-// 32-bit LDS addresses: stage bases are 256-byte aligned, so XOR-ing chunk
-// bits into a row address never carries into the row bits.
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p;
-}
-__device__ __forceinline__ bf16x8 lds_load16(uint32_t a) {
-  return *(__attribute__((address_space(3))) const bf16x8*)(uintptr_t)a;
-}
-__device__ __forceinline__ bf16x4 lds_read_tr_at(uint32_t a) {
-  return __builtin_bit_cast(bf16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                                        (__attribute__((address_space(3))) short4_t*)(uintptr_t)a));
-}
 
 // NQ: query-range slots the walk considers (2 when the call has at most two
 // query ranges, else kMaxQ); fewer slots keep the walk state in fewer registers.
@@ -291,11 +262,9 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
   };
 
   const float c = a.scale_log2;
-  // Per-lane parts of the swizzled LDS read addresses (see chunk_swz).
-  const uint32_t yrow = l32 * RB + ((half ^ chunk_swz<D>(l32)) * 16);
-  const int r0 = 4 * (G >> 1) + (sl >> 2), ch0 = 2 * (G & 1) + ((sl >> 1) & 1);
-  const uint32_t ytr0 = r0 * RB + ((ch0 ^ chunk_swz<D>(r0)) * 16) + 8 * (sl & 1);
-  const uint32_t ytr1 = (r0 + 8) * RB + ((ch0 ^ chunk_swz<D>(r0 + 8)) * 16) + 8 * (sl & 1);
+  // Per-lane parts of the swizzled LDS read addresses (device.hpp).
+  const uint32_t yrow = swz_row_part<D>(l32, half);
+  const uint32_t ytr0 = swz_tr_part<D>(G, sl, 0), ytr1 = swz_tr_part<D>(G, sl, 8);
   // One step of the walk on stage S: S = Q K^T, dP = dO V^T, P, dS, then
   // dV^T += dO^T P, dK^T += Q^T dS for every head of the pair.
   auto compute_step = [&](const Stage& S, const Cursor cu) __attribute__((always_inline)) {

@@ -22,13 +22,17 @@ constexpr float kLog2e = 1.44269504088896340736f;
 template <int D, int NW, bool HILO>
 __global__ __launch_bounds__(NW * 64) void bwd_dq_kernel(const AttnArgs a) {
   constexpr int BM = NW * 32, BN = 64, KS = D / 16, DT = D / 32;
-  // K and V row reads at pitch PB; K^T transpose reads from a second copy of K at pitch PT.
-  constexpr int PB = pitch_b128(D), PT = pitch_tr(D);
-  constexpr int NT = NW * 64;
-  constexpr int STAGE = BN * (2 * PB + PT);  // K tile, V tile, K tile again
-  __shared__ __attribute__((aligned(16))) bf16 lds[2 * STAGE];
+  // K and V tiles with swizzled rows: K serves both its row reads (S^T) and
+  // its transpose reads (K^T), V its row reads (dP^T).
+  constexpr uint32_t RB = D * 2, TB = BN * RB;
+  constexpr int STAGE = 2 * BN * D;
+  // Copies: each tile is BN * D / 8 16-byte slots, TI instructions of 64 lanes;
+  // waves 0 .. NW/2 - 1 copy K and the others V, IPW instructions each.
+  constexpr int TI = BN * D / 8 / 64, IPW = TI / (NW / 2);
+  static_assert(TI % (NW / 2) == 0, "whole copy instructions per wave");
+  __shared__ __attribute__((aligned(256))) bf16 lds[3 * STAGE];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, half = lane >> 5;
   const int G = lane >> 4, sl = lane & 15;
 
@@ -73,30 +77,59 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_kernel(const AttnArgs a) {
     for (int i = 0; i < 16; ++i) acc[d][i] = 0.f;
   const float c = a.scale_log2;
 
-  int j = 0, t = 0, t1 = 0, f0 = 0, f1 = 0;
-  bool have = find_key_tile(a, 0, qr.stream, pq0, pq1, BN, j, t, t1, f0, f1);
-  KVTileLoader<D, BN, NT> ld;
+  // Key tiles in visiting order: (key range j, tile t), the range's last
+  // visible tile t1 and its fully visible tiles [f0, f1).  Wave-uniform.
+  struct KCur {
+    int j, t, t1, f0, f1;
+    bool have;
+  };
+  auto next_tile = [&](KCur c) -> KCur {
+    if (!c.have) return c;
+    if (++c.t < c.t1) return c;
+    c.have = find_key_tile(a, c.j + 1, qr.stream, pq0, pq1, BN, c.j, c.t, c.t1, c.f0, c.f1);
+    return c;
+  };
+  // LDS-DMA copy of a tile into stage st (empty copies past the last tile, so
+  // every wave issues IPW per tile); rows past the range end read zeros.
+  const int64_t HKV = a.kv_heads;
+  uint32_t voff[IPW];
+  const int cw = w % (NW / 2);
+#pragma unroll
+  for (int i = 0; i < IPW; ++i) voff[i] = swz_src_offset<D>((cw * IPW + i) * 64 + lane, HKV * D);
+  auto copy_tile = [&](bf16* st, const KCur cc) __attribute__((always_inline)) {
+    const KRangeArg& kr = a.kr[cc.have ? cc.j : 0];
+    const int nrows = cc.have ? imin(BN, kr.len - cc.t * BN) : 0;
+    const int64_t eoff = (((int64_t)it.b * kr.bstride + (int64_t)cc.t * BN) * HKV + kvh) * D;
+    const uint32_t bytes = cc.have ? (uint32_t)(((int64_t)(nrows - 1) * HKV * D + D) * 2) : 0u;
+    const auto r = make_rsrc((const bf16*)(w < NW / 2 ? kr.k : kr.v) + (cc.have ? eoff : 0), bytes);
+    bf16* dst = st + (w < NW / 2 ? 0 : BN * D) + cw * IPW * 512;
+#pragma unroll
+    for (int i = 0; i < IPW; ++i) buf_to_lds<16>(r, dst + i * 512, voff[i], 0);
+  };
+  // Per-lane parts of the swizzled read addresses (device.hpp).
+  const uint32_t yrow = swz_row_part<D>(l32, half);
+  const uint32_t ytr0 = swz_tr_part<D>(G, sl, 0), ytr1 = swz_tr_part<D>(G, sl, 8);
+
+  // Three LDS stages, copies two tiles ahead (as in the forward).
+  KCur c0;
+  c0.have = find_key_tile(a, 0, qr.stream, pq0, pq1, BN, c0.j, c0.t, c0.t1, c0.f0, c0.f1);
+  KCur c1 = next_tile(c0), c2 = next_tile(c1);
+  copy_tile(lds, c0);
+  copy_tile(lds + STAGE, c1);
+  vm_wait_barrier<IPW>();
   int cur = 0;
   int lane_lo = 0, lane_w = 0, lane_j = -1;
-  if (have) {
-    ld.load(a, j, t, it.b, kvh, tid);
-    ld.template store<PB, PB, PT>(lds, lds + BN * PB, tid, lds + 2 * BN * PB);
-  }
-  __syncthreads();
-
-  while (have) {
-    int jn = j, tn = t + 1, t1n = t1, f0n = f0, f1n = f1;
-    bool have_next = tn < t1;
-    if (!have_next) have_next = find_key_tile(a, j + 1, qr.stream, pq0, pq1, BN, jn, tn, t1n, f0n, f1n);
-    if (have_next) ld.load(a, jn, tn, it.b, kvh, tid);
+  while (c0.have) {
+    copy_tile(lds + (cur == 0 ? 2 : cur - 1) * STAGE, c2);
+    const int j = c0.j, t = c0.t, f0 = c0.f0, f1 = c0.f1;
     if (lane_j != j) {
       lane_key_interval(a, j, qr.stream, pq, lane_lo, lane_w);
       lane_j = j;
     }
 
-    const bf16* Ks = lds + cur * STAGE;
-    const bf16* Vs = Ks + BN * PB;
-    const bf16* Kt = Ks + 2 * BN * PB;
+    // S^T = K Q^T and dP^T = V dO^T: K and V rows 32u + l32 by row reads.
+    const uint32_t sb = lds_addr(lds + cur * STAGE);
+    const uint32_t zr = sb + yrow;
     f32x16 sacc[2], dpacc[2];
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
@@ -105,12 +138,11 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_kernel(const AttnArgs a) {
         sacc[u][i] = 0.f;
         dpacc[u][i] = 0.f;
       }
-      const bf16* kp = Ks + (u * 32 + l32) * PB + 8 * half;
-      const bf16* vp = Vs + (u * 32 + l32) * PB + 8 * half;
 #pragma unroll
       for (int s = 0; s < KS; ++s) {
-        sacc[u] = mfma32(*(const bf16x8*)(kp + 16 * s), qf[s], sacc[u]);
-        dpacc[u] = mfma32(*(const bf16x8*)(vp + 16 * s), df[s], dpacc[u]);
+        const uint32_t ad = (zr ^ (32u * s)) + u * 32 * RB;
+        sacc[u] = mfma32(lds_load16(ad), qf[s], sacc[u]);
+        dpacc[u] = mfma32(lds_load16(ad + TB), df[s], dpacc[u]);
       }
     }
 
@@ -140,26 +172,27 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_kernel(const AttnArgs a) {
       }
 
     // dQ^T[d][q] += sum_key K[key][d] dS[q][key]; key order per 16-key step as in the forward.
+    const uint32_t zt0 = sb + ytr0, zt1 = sb + ytr1;  // K tile by transpose reads
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      const bf16* kp = Kt + (16 * u + 4 * (G >> 1) + (sl >> 2)) * PT + 16 * (G & 1) + 4 * (sl & 3);
 #pragma unroll
       for (int d = 0; d < DT; ++d) {
-        const bf16x8 ka = cat(lds_read_tr(kp + 32 * d), lds_read_tr(kp + 32 * d + 8 * PT));
+        const bf16x8 ka = cat(lds_read_tr_at((zt0 ^ (64u * d)) + u * 16 * RB),
+                              lds_read_tr_at((zt1 ^ (64u * d)) + u * 16 * RB));
         acc[d] = mfma32(ka, dsb[u], acc[d]);
         if constexpr (HILO) acc[d] = mfma32(ka, dsl[u], acc[d]);
       }
     }
 
-    if (have_next) {
-      bf16* st = lds + (cur ^ 1) * STAGE;
-      ld.template store<PB, PB, PT>(st, st + BN * PB, tid, st + 2 * BN * PB);
-    }
-    __syncthreads();
-    cur ^= 1;
-    j = jn; t = tn; t1 = t1n; f0 = f0n; f1 = f1n;
-    have = have_next;
+    vm_wait_barrier<IPW>();
+    cur = cur == 2 ? 0 : cur + 1;
+    c0 = c1;
+    c1 = c2;
+    c2 = next_tile(c2);
   }
+  // Copies still in flight target stages nobody reads; they must land before
+  // the workgroup's LDS is released.
+  __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
 
   if (row_ok) {
     const int64_t orow = (((int64_t)it.b * qr.bstride + my_row) * H + it.h) * D;

@@ -19,15 +19,6 @@ namespace bdlm {
 
 enum : int { kClean = 0, kCorrupted = 1 };
 enum : int { kIntraCausal = 0, kIntraBlock = 1 };
-// LDS row pitches (in bf16 elements) of D-wide tiles.  gfx950 LDS has 64 banks of
-// 4 bytes; a 16-byte row read (ds_read_b128, lanes 0..15 on 16 consecutive rows)
-// is conflict-free when consecutive rows start 4 banks apart modulo 64, and a
-// transpose read (ds_read_b64_tr_b16, lanes 0..31 on 4 consecutive rows x 64
-// bytes) when they start 16 banks apart.  No single pitch serves both, so a tile
-// read both ways is kept in LDS twice, one copy per pitch (measured: 288-byte
-// rows, D + 16, conflict 2-way on both).
-constexpr int pitch_b128(int d) { return d + 8; }
-constexpr int pitch_tr(int d) { return d + 32; }
 
 constexpr int kMaxQ = 4;
 constexpr int kMaxK = 32;

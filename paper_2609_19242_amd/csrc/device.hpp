@@ -65,12 +65,63 @@ __device__ __forceinline__ void vm_wait_barrier() {
   asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(N) : "memory");
 }
 
-// Transposed 8-byte LDS read (see the header comment).  p must point into LDS.
-__device__ __forceinline__ bf16x4 lds_read_tr(const bf16* p) {
-  typedef __attribute__((address_space(3))) short4_t lds_s4;
-  typedef __attribute__((address_space(3))) bf16 lds_bf16;
-  short4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4*)(lds_bf16*)p);
-  return __builtin_bit_cast(bf16x4, v);
+// ---- swizzled LDS tiles of bf16 rows.
+//
+// Tiles of D-element bf16 rows (Q, dO, K or V) are stored in LDS unpadded;
+// logical 16-byte chunk c of row r sits in physical chunk c ^ chunk_swz<D>(r).
+// The kernels read such a tile in two patterns: 64-lane ds_read_b128 row reads
+// (16 lanes per LDS cycle: 16 consecutive rows, one chunk each) and
+// ds_read_b64_tr_b16 transpose reads (32 lanes per cycle: 4 consecutive rows,
+// 64 bytes each).  With 256-byte rows (D = 128) the 16 rows of a row read land
+// in 16 distinct chunk columns and the 4 rows of a transpose read in 4
+// disjoint quarter-rows, so both are conflict-free (64 banks x 4 bytes); for
+// D = 64 (128-byte rows, two rows per bank period) the same holds with the
+// second function.  Padding alone cannot do both: 272-byte rows are 4-way on
+// transpose reads, 320-byte rows 4-way on row reads, 288-byte rows 2-way on
+// each.  The function depends on r mod 16 only.  Copies into such a tile go
+// through LDS DMA (buf_to_lds), where lane i fills physical slot i of its
+// instruction: the lane fetches the logical chunk that belongs there.
+template <int D>
+__host__ __device__ constexpr int chunk_swz(int r) {
+  return D == 128 ? (((r & 3) << 2) | ((r >> 2) & 3)) : ((((r >> 1) & 1) << 2) | ((r >> 2) & 3));
+}
+
+// Global byte offset of the logical chunk stored in physical slot `slot` of a
+// swizzled tile whose row r lives at global element offset r * row_stride.
+template <int D>
+__device__ __forceinline__ uint32_t swz_src_offset(int slot, int64_t row_stride) {
+  const int row = slot / (D / 8), ch = (slot % (D / 8)) ^ chunk_swz<D>(row);
+  return (uint32_t)((row * row_stride + ch * 8) * 2);
+}
+
+// 32-bit LDS addresses.  Tile bases are 256-byte aligned, so XOR-ing chunk
+// bits into a row address never carries into the row bits.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p;
+}
+__device__ __forceinline__ bf16x8 lds_load16(uint32_t a) {
+  return *(__attribute__((address_space(3))) const bf16x8*)(uintptr_t)a;
+}
+// Transposed 8-byte LDS read at LDS address a (see the header comment).
+__device__ __forceinline__ bf16x4 lds_read_tr_at(uint32_t a) {
+  return __builtin_bit_cast(bf16x4, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                                        (__attribute__((address_space(3))) short4_t*)(uintptr_t)a));
+}
+
+// Per-lane parts of the swizzled read addresses.  Row reads: lane (half, l32)
+// reads logical chunk 2k + half of row l32 at (base + row_part) ^ 32k.
+// Transpose reads of the MFMA fragment layout: the lane reads rows 16u + r0
+// and 16u + r0 + 8 (r0 = 4 (G >> 1) + (sl >> 2)), 8-byte piece
+// 8d + 4 (G & 1) + (sl & 3), at (base + tr_part(0 or 8)) ^ 64d; row offsets
+// that are multiples of 16 rows are plain additions.
+template <int D>
+__device__ __forceinline__ uint32_t swz_row_part(int l32, int half) {
+  return l32 * (2 * D) + ((half ^ chunk_swz<D>(l32)) * 16);
+}
+template <int D>
+__device__ __forceinline__ uint32_t swz_tr_part(int G, int sl, int plus) {
+  const int r = 4 * (G >> 1) + (sl >> 2) + plus, ch = 2 * (G & 1) + ((sl >> 1) & 1);
+  return r * (2 * D) + ((ch ^ chunk_swz<D>(r)) * 16) + 8 * (sl & 1);
 }
 
 __device__ __forceinline__ bf16x8 cat(bf16x4 a, bf16x4 b) {

@@ -32,12 +32,15 @@ constexpr float kSlack = 8.f;  // largest exponent p = exp2(s c - m_run) may rea
 template <int D, int NW, bool HILO>
 __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
   constexpr int BM = NW * 32, BN = 64, KS = D / 16, DT = D / 32;
-  constexpr int PK = pitch_b128(D), PV = pitch_tr(D);  // K: row reads; V: transpose reads
-  constexpr int NT = NW * 64;
-  constexpr int STAGE = BN * (PK + PV);  // K tile + V tile
-  __shared__ __attribute__((aligned(16))) bf16 lds[2 * STAGE];
+  constexpr uint32_t RB = D * 2, TB = BN * RB;  // row and tile bytes in LDS
+  constexpr int STAGE = 2 * BN * D;             // K tile + V tile (elements), swizzled rows
+  // Copies: each tile is BN * D / 8 16-byte slots, TI instructions of 64 lanes;
+  // waves 0 .. NW/2 - 1 copy K and the others V, IPW instructions each.
+  constexpr int TI = BN * D / 8 / 64, IPW = TI / (NW / 2);
+  static_assert(TI % (NW / 2) == 0, "whole copy instructions per wave");
+  __shared__ __attribute__((aligned(256))) bf16 lds[3 * STAGE];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, half = lane >> 5;
   const int G = lane >> 4, sl = lane & 15;
 
@@ -70,41 +73,68 @@ __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
   float m_run = -INFINITY, l_run = 0.f;
   const float c = a.scale_log2;
 
-  // Uniform iteration state over (key range j, tile t).
-  int j = 0, t = 0, t1 = 0, f0 = 0, f1 = 0;
-  bool have = find_key_tile(a, 0, qr.stream, pq0, pq1, BN, j, t, t1, f0, f1);
-  KVTileLoader<D, BN, NT> ld;
+  // Key tiles in visiting order: (key range j, tile t), the range's last
+  // visible tile t1 and its fully visible tiles [f0, f1).  Wave-uniform.
+  struct KCur {
+    int j, t, t1, f0, f1;
+    bool have;
+  };
+  auto next_tile = [&](KCur c) -> KCur {
+    if (!c.have) return c;
+    if (++c.t < c.t1) return c;
+    c.have = find_key_tile(a, c.j + 1, qr.stream, pq0, pq1, BN, c.j, c.t, c.t1, c.f0, c.f1);
+    return c;
+  };
+  // LDS-DMA copy of a tile into stage st (empty copies past the last tile, so
+  // every wave issues IPW per tile); rows past the range end read zeros.
+  uint32_t voff[IPW];
+  const int cw = w % (NW / 2);
+#pragma unroll
+  for (int i = 0; i < IPW; ++i) voff[i] = swz_src_offset<D>((cw * IPW + i) * 64 + lane, HKV * D);
+  auto copy_tile = [&](bf16* st, const KCur c) __attribute__((always_inline)) {
+    const KRangeArg& kr = a.kr[c.have ? c.j : 0];
+    const int nrows = c.have ? imin(BN, kr.len - c.t * BN) : 0;
+    const int64_t eoff = (((int64_t)it.b * kr.bstride + (int64_t)c.t * BN) * HKV + kvh) * D;
+    const uint32_t bytes = c.have ? (uint32_t)(((int64_t)(nrows - 1) * HKV * D + D) * 2) : 0u;
+    const auto r = make_rsrc((const bf16*)(w < NW / 2 ? kr.k : kr.v) + (c.have ? eoff : 0), bytes);
+    bf16* dst = st + (w < NW / 2 ? 0 : BN * D) + cw * IPW * 512;
+#pragma unroll
+    for (int i = 0; i < IPW; ++i) buf_to_lds<16>(r, dst + i * 512, voff[i], 0);
+  };
+  // Per-lane parts of the swizzled read addresses (device.hpp).
+  const uint32_t yrow = swz_row_part<D>(l32, half);
+  const uint32_t ytr0 = swz_tr_part<D>(G, sl, 0), ytr1 = swz_tr_part<D>(G, sl, 8);
 
+  // Three LDS stages, copies two tiles ahead.  At the barrier closing a tile,
+  // every wave has waited for its copies of the next tile (only those of the
+  // tile after it stay in flight) and has finished reading the stage the
+  // following copies overwrite.
+  KCur c0;
+  c0.have = find_key_tile(a, 0, qr.stream, pq0, pq1, BN, c0.j, c0.t, c0.t1, c0.f0, c0.f1);
+  KCur c1 = next_tile(c0), c2 = next_tile(c1);
+  copy_tile(lds, c0);
+  copy_tile(lds + STAGE, c1);
+  vm_wait_barrier<IPW>();
   int cur = 0;
   int lane_lo = 0, lane_w = 0, lane_j = -1;
-  if (have) {
-    ld.load(a, j, t, it.b, kvh, tid);
-    ld.template store<PK, PV>(lds, lds + BN * PK, tid);
-  }
-  __syncthreads();
-
-  while (have) {
-    // Next tile (possibly in a later key range), prefetched into registers.
-    int jn = j, tn = t + 1, t1n = t1, f0n = f0, f1n = f1;
-    bool have_next = tn < t1;
-    if (!have_next) have_next = find_key_tile(a, j + 1, qr.stream, pq0, pq1, BN, jn, tn, t1n, f0n, f1n);
-    if (have_next) ld.load(a, jn, tn, it.b, kvh, tid);
-
+  while (c0.have) {
+    copy_tile(lds + (cur == 0 ? 2 : cur - 1) * STAGE, c2);
+    const int j = c0.j, t = c0.t, f0 = c0.f0, f1 = c0.f1;
     if (lane_j != j) {  // this lane's visible key interval inside range j
       lane_key_interval(a, j, qr.stream, pq, lane_lo, lane_w);
       lane_j = j;
     }
 
-    const bf16* Ks = lds + cur * STAGE;
-    const bf16* Vs = Ks + BN * PK;
+    // S^T = K Q^T: K rows 32u + l32 by row reads (K tile at the stage base).
+    const uint32_t sb = lds_addr(lds + cur * STAGE);
+    const uint32_t zr = sb + yrow;
     f32x16 sacc[2];
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) sacc[u][i] = 0.f;
-      const bf16* kp = Ks + (u * 32 + l32) * PK + 8 * half;
 #pragma unroll
-      for (int s = 0; s < KS; ++s) sacc[u] = mfma32(*(const bf16x8*)(kp + 16 * s), qf[s], sacc[u]);
+      for (int s = 0; s < KS; ++s) sacc[u] = mfma32(lds_load16((zr ^ (32u * s)) + u * 32 * RB), qf[s], sacc[u]);
     }
 
     if (!(t >= f0 && t < f1)) {
@@ -157,23 +187,27 @@ __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
 
     // O^T[d][q] += sum_key V[key][d] P[q][key]; the key order inside each
     // 16-key step follows the S^T register layout (see device.hpp).
+    const uint32_t zt0 = sb + TB + ytr0, zt1 = sb + TB + ytr1;  // V tile by transpose reads
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      const bf16* vp = Vs + (16 * u + 4 * (G >> 1) + (sl >> 2)) * PV + 16 * (G & 1) + 4 * (sl & 3);
 #pragma unroll
       for (int d = 0; d < DT; ++d) {
-        const bf16x8 va = cat(lds_read_tr(vp + 32 * d), lds_read_tr(vp + 32 * d + 8 * PV));
+        const bf16x8 va = cat(lds_read_tr_at((zt0 ^ (64u * d)) + u * 16 * RB),
+                              lds_read_tr_at((zt1 ^ (64u * d)) + u * 16 * RB));
         acc[d] = mfma32(va, pb[u], acc[d]);
         if constexpr (HILO) acc[d] = mfma32(va, pl[u], acc[d]);
       }
     }
 
-    if (have_next) ld.template store<PK, PV>(lds + (cur ^ 1) * STAGE, lds + (cur ^ 1) * STAGE + BN * PK, tid);
-    __syncthreads();
-    cur ^= 1;
-    j = jn; t = tn; t1 = t1n; f0 = f0n; f1 = f1n;
-    have = have_next;
+    vm_wait_barrier<IPW>();
+    cur = cur == 2 ? 0 : cur + 1;
+    c0 = c1;
+    c1 = c2;
+    c2 = next_tile(c2);
   }
+  // Copies still in flight target stages nobody reads; they must land before
+  // the workgroup's LDS is released.
+  __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
 
   // Epilogue: O = O^T / l (bf16), LSE = ln(2) * (m + log2 l); empty rows O = 0, LSE = -inf.
   const float l_tot = l_run + partner(l_run);

@@ -92,46 +92,4 @@ __device__ inline void lane_key_interval(const AttnArgs& a, int j, int qs, int p
   w = imax(h - l, 0);
 }
 
-// Global -> register -> LDS staging of one BN-row tile of two [rows][HKV][D]
-// bf16 tensors (K and V) of key range j.  Rows past the range read as zero.
-template <int D, int BN, int NT>
-struct KVTileLoader {
-  static constexpr int CPR = D / 8;
-  static constexpr int CPT = BN * CPR / NT;
-  static_assert((BN * CPR) % NT == 0, "tile chunks must divide evenly");
-  u32x4 pk[CPT], pv[CPT];
-
-  __device__ inline void load(const AttnArgs& a, int j, int t, int b, int kvh, int tid) {
-    const KRangeArg& kr = a.kr[j];
-    const int64_t HKV = a.kv_heads;
-    const int nrows = imin(BN, kr.len - t * BN);
-    const int64_t eoff = (((int64_t)b * kr.bstride + (int64_t)t * BN) * HKV + kvh) * D;
-    const uint32_t bytes = (uint32_t)(((int64_t)(nrows - 1) * HKV * D + D) * 2);
-    const auto rk = make_rsrc((const bf16*)kr.k + eoff, bytes);
-    const auto rv = make_rsrc((const bf16*)kr.v + eoff, bytes);
-#pragma unroll
-    for (int n = 0; n < CPT; ++n) {
-      const int cidx = tid + n * NT;
-      const int row = cidx / CPR, col = cidx % CPR;
-      const uint32_t off = (uint32_t)(((int64_t)row * HKV * D + col * 8) * 2);
-      pk[n] = buf_load16(rk, off);
-      pv[n] = buf_load16(rv, off);
-    }
-  }
-
-  // K rows to ks at pitch PK, V rows to vs at pitch PV, and (when k2 is not
-  // null) K a second time to k2 at pitch PK2.
-  template <int PK, int PV, int PK2 = PK>
-  __device__ inline void store(bf16* ks, bf16* vs, int tid, bf16* k2 = nullptr) const {
-#pragma unroll
-    for (int n = 0; n < CPT; ++n) {
-      const int cidx = tid + n * NT;
-      const int row = cidx / CPR, col = cidx % CPR;
-      *(u32x4*)(ks + row * PK + col * 8) = pk[n];
-      *(u32x4*)(vs + row * PV + col * 8) = pv[n];
-      if (k2) *(u32x4*)(k2 + row * PK2 + col * 8) = pk[n];
-    }
-  }
-};
-
 }  // namespace bdlm
