@@ -18,6 +18,24 @@
  * range, the J-way log-sum-exp merge of partials (eq:csbp-lse-merge), and the
  * exact backward from the saved output and LSE (App. C, fused backward).
  *
+ * Mask generalisations (both keep every visible set an interval of positions):
+ *  - window W > 0 (the sliding-window attention layers of the paper's
+ *    DiffusionGemma runs, App. "Savings Breakdowns"): with e the end of the
+ *    clean context the rules above give a query (q + 1 for a clean query under
+ *    the token-causal rule, the end of its block under BDLM_CLEAN_INTRA_BLOCK,
+ *    the start of its block for a corrupted query), only clean keys k with
+ *    e - W <= k < e stay visible.  Corrupted keys are unaffected.
+ *  - clean_prefix (the DFlash2 drafter attention, App. "DFlash2 Drafter
+ *    Training Methodology", eq:dflash2-block-attention): corrupted block b is a
+ *    draft block whose clean context (the target features) ends at
+ *    clean_prefix[b] = a_b instead of at block_size * b; it still sees its own
+ *    block bidirectionally.  The table must be non-decreasing with entries in
+ *    [0, L] (draft blocks ordered by anchor: their losses are independent, so
+ *    the order is free).  The asynchronous calls cannot check the contents:
+ *    entries are clamped into [0, L] when read, and a decreasing table gives an
+ *    unspecified mask (never an out-of-bounds access).  bdlm_visible_pairs
+ *    checks the table and returns -1 when it breaks the contract.
+ *
  * Rows and ranges.  A tensor's rows are described by bdlm_range records: a
  * range is `len` consecutive rows of one stream holding global positions
  * [pos0, pos0 + len).  Per batch element b, row i of a range lives at row
@@ -94,6 +112,11 @@ typedef struct {
                          two-term bf16 sum hi + lo (about 16 significant bits, up to 1.5x the
                          matrix work of those products), for inputs with large scores or |dS|,
                          e.g. keys of large norm.  Ignored by the fp32 path. */
+  int64_t window;     /* 0: no limit.  > 0: a query sees only the last `window` positions of its clean
+                         context (sliding-window layers; see "Mask generalisations" below) */
+  const int32_t* clean_prefix; /* NULL, or a device array of L / block_size ints: the end of the clean
+                         context of corrupted block b (DFlash2 anchors; see below).  Read by the kernels
+                         during the call's execution; bdlm_visible_pairs reads it synchronously. */
 } bdlm_problem;
 
 /* A run of rows of one stream (see "Rows and ranges" above). */

@@ -62,7 +62,8 @@ def joint_ranges(L: int) -> List[Tuple[int, int, int]]:
     return [(CORRUPTED, 0, L), (CLEAN, 0, L)]
 
 
-def visible(q_stream, q_pos, k_stream, k_pos, M: int, clean_intra: int = CLEAN_INTRA_CAUSAL) -> np.ndarray:
+def visible(q_stream, q_pos, k_stream, k_pos, M: int, clean_intra: int = CLEAN_INTRA_CAUSAL,
+            window: int = 0, clean_prefix: Optional[Sequence[int]] = None) -> np.ndarray:
     """Explicit BDLM mask ``mask[i, j]``: may query row i attend to key row j?
 
     Rules (Sec. 3.2; App. A step 1):
@@ -76,6 +77,18 @@ def visible(q_stream, q_pos, k_stream, k_pos, M: int, clean_intra: int = CLEAN_I
     * corrupted query, clean key: the clean prefix of earlier blocks,
       block(key) < block(query);
     * clean query, corrupted key: never.
+
+    Two generalisations (the library's ``window`` and ``clean_prefix``):
+
+    * ``clean_prefix[b]`` (DFlash2 drafter attention, App. "DFlash2 Drafter
+      Training Methodology", eq. ``eq:dflash2-block-attention``): corrupted
+      block b is a draft block that sees the clean rows (target features)
+      before its anchor ``a_b = clean_prefix[b]`` instead of before ``M * b``;
+    * ``window > 0`` (the sliding-window layers of App. "Savings Breakdowns";
+      the paper gives only the width, this is the reading): with ``e`` the end
+      of the clean context a query sees under the rules above (``q + 1``, the
+      end of its block under the block reading, ``M * b`` or ``a_b`` for a
+      corrupted query), only clean keys ``e - window <= k < e`` stay visible.
     """
     qs = np.asarray(q_stream)[:, None]
     qp = np.asarray(q_pos)[:, None]
@@ -85,12 +98,23 @@ def visible(q_stream, q_pos, k_stream, k_pos, M: int, clean_intra: int = CLEAN_I
     kb = kp // M
     if clean_intra == CLEAN_INTRA_CAUSAL:
         clean_clean = kp <= qp
+        clean_end = qp + 1
     elif clean_intra == CLEAN_INTRA_BLOCK:
         clean_clean = kb <= qb
+        clean_end = (qb + 1) * M
     else:
         raise ValueError(f"unknown clean_intra {clean_intra}")
     corr_corr = kb == qb
-    corr_clean = kb < qb
+    if clean_prefix is None:
+        corr_clean = kb < qb
+        corr_end = qb * M
+    else:
+        table = np.asarray(clean_prefix, dtype=np.int64)
+        corr_end = table[np.minimum(qb, table.shape[0] - 1)]
+        corr_clean = kp < corr_end
+    if window:
+        clean_clean = clean_clean & (kp >= clean_end - window)
+        corr_clean = corr_clean & (kp >= corr_end - window)
     return np.where(
         qs == CLEAN,
         np.where(ks == CLEAN, clean_clean, False),
@@ -151,7 +175,8 @@ def _heads_arg(heads: Optional[Iterable[int]], Hq: int) -> List[int]:
 
 def fwd(q, k, v, q_ranges, k_ranges, M: int, clean_intra: int = CLEAN_INTRA_CAUSAL,
         scale: Optional[float] = None, heads: Optional[Iterable[int]] = None,
-        q_rows: Optional[np.ndarray] = None, chunk: int = 1024):
+        q_rows: Optional[np.ndarray] = None, chunk: int = 1024, window: int = 0,
+        clean_prefix: Optional[Sequence[int]] = None):
     """Masked attention of the query rows over all key rows.
 
     ``q`` is ``[batch][n_q][Hq][d]`` holding ``q_ranges``; ``k``/``v`` are
@@ -174,7 +199,7 @@ def fwd(q, k, v, q_ranges, k_ranges, M: int, clean_intra: int = CLEAN_INTRA_CAUS
     LSE = np.full((B, len(hs), rows.shape[0]), -np.inf)
     for c0 in range(0, rows.shape[0], chunk):
         r = rows[c0:c0 + chunk]
-        mask = visible(qs_all[r], qp_all[r], ks, kp, M, clean_intra)
+        mask = visible(qs_all[r], qp_all[r], ks, kp, M, clean_intra, window, clean_prefix)
         for b in range(B):
             for hi, h in enumerate(hs):
                 o, lse = attention_fwd_head(q[b, r, h], k[b, :, h // g], v[b, :, h // g], mask, scale)
@@ -184,7 +209,8 @@ def fwd(q, k, v, q_ranges, k_ranges, M: int, clean_intra: int = CLEAN_INTRA_CAUS
 
 
 def bwd(q, k, v, o, lse, do, q_ranges, k_ranges, M: int, clean_intra: int = CLEAN_INTRA_CAUSAL,
-        scale: Optional[float] = None, heads: Optional[Iterable[int]] = None, chunk: int = 1024):
+        scale: Optional[float] = None, heads: Optional[Iterable[int]] = None, chunk: int = 1024,
+        window: int = 0, clean_prefix: Optional[Sequence[int]] = None):
     """Gradients of ``sum(dO * O)`` given the saved forward ``(O, LSE)``.
 
     ``o``/``do`` are ``[batch][n_q][len(heads)][d]`` and ``lse`` is
@@ -207,7 +233,7 @@ def bwd(q, k, v, o, lse, do, q_ranges, k_ranges, M: int, clean_intra: int = CLEA
     dV = np.zeros(v.shape)
     for c0 in range(0, nq, chunk):
         r = slice(c0, min(nq, c0 + chunk))
-        mask = visible(qs_all[r], qp_all[r], ks, kp, M, clean_intra)
+        mask = visible(qs_all[r], qp_all[r], ks, kp, M, clean_intra, window, clean_prefix)
         for b in range(B):
             for hi, h in enumerate(hs):
                 kv = h // g
@@ -260,11 +286,13 @@ def joint_bwd(q, k, v, o, lse, do, L: int, M: int, **kw):
     return bwd(q, k, v, o, lse, do, r, r, M, **kw)
 
 
-def count_visible_pairs(q_ranges, k_ranges, M: int, clean_intra: int = CLEAN_INTRA_CAUSAL, chunk: int = 4096) -> int:
+def count_visible_pairs(q_ranges, k_ranges, M: int, clean_intra: int = CLEAN_INTRA_CAUSAL, chunk: int = 4096,
+                        window: int = 0, clean_prefix: Optional[Sequence[int]] = None) -> int:
     """Popcount of the explicit mask: the number of valid query-key pairs per (batch, head)."""
     qs, qp = rows_of(q_ranges)
     ks, kp = rows_of(k_ranges)
     total = 0
     for c0 in range(0, qs.shape[0], chunk):
-        total += int(visible(qs[c0:c0 + chunk], qp[c0:c0 + chunk], ks, kp, M, clean_intra).sum())
+        total += int(visible(qs[c0:c0 + chunk], qp[c0:c0 + chunk], ks, kp, M, clean_intra, window,
+                             clean_prefix).sum())
     return total

@@ -44,6 +44,7 @@ class Problem(ctypes.Structure):
         ("heads", ctypes.c_int32), ("kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
         ("dtype", ctypes.c_int32), ("scale", ctypes.c_float), ("clean_intra", ctypes.c_int32),
         ("out_f32", ctypes.c_int32), ("hilo", ctypes.c_int32),
+        ("window", ctypes.c_int64), ("clean_prefix", ctypes.c_void_p),
     ]
 
 
@@ -150,10 +151,20 @@ def _dtype_code(dt: torch.dtype) -> int:
 
 def make_problem(batch: int, L: int, block_size: int, heads: int, kv_heads: int, head_dim: int,
                  dtype, scale: float = 0.0, clean_intra: int = CLEAN_INTRA_CAUSAL, out_f32: bool = False,
-                 hilo: bool = False) -> Problem:
+                 hilo: bool = False, window: int = 0, clean_prefix: Optional[torch.Tensor] = None) -> Problem:
+    """Problem record.  ``window`` limits every query to the last ``window`` positions of its clean
+    context (0: no limit); ``clean_prefix`` is an int32 device tensor of ``L // block_size`` entries,
+    the end of corrupted block b's clean context (DFlash2 anchors), kept alive by the caller until the
+    kernels that use it have run."""
     code = dtype if isinstance(dtype, int) else _dtype_code(dtype)
+    pref = None
+    if clean_prefix is not None:
+        if clean_prefix.dtype != torch.int32 or not clean_prefix.is_cuda or not clean_prefix.is_contiguous() \
+                or clean_prefix.numel() != L // block_size:
+            raise ValueError("clean_prefix must be a contiguous int32 device tensor of L // block_size entries")
+        pref = clean_prefix.data_ptr()
     return Problem(batch, L, block_size, heads, kv_heads, head_dim, code, scale, clean_intra, int(bool(out_f32)),
-                   int(bool(hilo)))
+                   int(bool(hilo)), int(window), pref)
 
 
 def joint_ranges(L: int) -> List[Range]:
@@ -233,7 +244,8 @@ def _check_joint(q, k, v):
 
 
 def joint_fwd(q, k, v, block_size: int, clean_intra: int = CLEAN_INTRA_CAUSAL, scale: float = 0.0,
-              out_f32: bool = False, out: Optional[tuple] = None, stream=None, hilo: bool = False):
+              out_f32: bool = False, out: Optional[tuple] = None, stream=None, hilo: bool = False,
+              window: int = 0, clean_prefix: Optional[torch.Tensor] = None):
     """Fused forward over packed ``[x_t ; x]`` tensors ``q [B][2L][Hq][D]``, ``k, v [B][2L][Hkv][D]``.
 
     Returns ``(o, lse)`` with ``lse [B][Hq][2L]`` fp32; ``o`` is fp32 when ``out_f32``.
@@ -241,7 +253,8 @@ def joint_fwd(q, k, v, block_size: int, clean_intra: int = CLEAN_INTRA_CAUSAL, s
     _check_joint(q, k, v)
     B, n, Hq, D = q.shape
     L = n // 2
-    p = make_problem(B, L, block_size, Hq, k.shape[2], D, q.dtype, scale, clean_intra, out_f32, hilo)
+    p = make_problem(B, L, block_size, Hq, k.shape[2], D, q.dtype, scale, clean_intra, out_f32, hilo,
+                     window, clean_prefix)
     odt = torch.float32 if out_f32 else q.dtype
     o, lse = out if out is not None else (torch.empty(q.shape, dtype=odt, device=q.device),
                                           torch.empty((B, Hq, n), dtype=torch.float32, device=q.device))
@@ -253,12 +266,13 @@ def joint_fwd(q, k, v, block_size: int, clean_intra: int = CLEAN_INTRA_CAUSAL, s
 
 def joint_bwd(q, k, v, o, lse, do, block_size: int, clean_intra: int = CLEAN_INTRA_CAUSAL, scale: float = 0.0,
               out_f32: bool = False, out: Optional[tuple] = None, workspace: Optional[torch.Tensor] = None,
-              stream=None, hilo: bool = False):
+              stream=None, hilo: bool = False, window: int = 0, clean_prefix: Optional[torch.Tensor] = None):
     """Backward of :func:`joint_fwd`; returns ``(dq, dk, dv)`` (fp32 when ``out_f32``; ``o`` must match)."""
     _check_joint(q, k, v)
     B, n, Hq, D = q.shape
     L = n // 2
-    p = make_problem(B, L, block_size, Hq, k.shape[2], D, q.dtype, scale, clean_intra, out_f32, hilo)
+    p = make_problem(B, L, block_size, Hq, k.shape[2], D, q.dtype, scale, clean_intra, out_f32, hilo,
+                     window, clean_prefix)
     r = joint_ranges(L)
     odt = torch.float32 if out_f32 else q.dtype
     if o.dtype != odt:

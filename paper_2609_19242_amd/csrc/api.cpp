@@ -93,7 +93,15 @@ bdlm_status check_problem(const bdlm_problem* p) {
   if (!std::isfinite(p->scale)) return fail(BDLM_ERR_INVALID, "scale is not finite");
   if (p->out_f32 != 0 && p->out_f32 != 1) return fail(BDLM_ERR_INVALID, "out_f32 must be 0 or 1");
   if (p->hilo != 0 && p->hilo != 1) return fail(BDLM_ERR_INVALID, "hilo must be 0 or 1");
+  if (p->window < 0 || p->window >= kMaxPos)
+    return fail(BDLM_ERR_INVALID, "window must be in [0, 2^30) (got %lld)", (long long)p->window);
+  if (p->clean_prefix && (reinterpret_cast<uintptr_t>(p->clean_prefix) & 3u) != 0)
+    return fail(BDLM_ERR_INVALID, "clean_prefix is not 4-byte aligned");
   return BDLM_OK;
+}
+
+MaskRule host_rule(const bdlm_problem* p, const int* prefix) {
+  return MaskRule{(int)p->block_size, p->clean_intra, (int)p->window, (int)(p->L / p->block_size), (int)p->L, prefix};
 }
 
 bdlm_status check_range(const bdlm_problem* p, const bdlm_range& r, const char* what, int idx) {
@@ -129,6 +137,10 @@ void fill_common(AttnArgs& a, const bdlm_problem* p) {
   a.group = p->heads / p->kv_heads;
   a.M = (int32_t)p->block_size;
   a.intra = p->clean_intra;
+  a.window = (int32_t)p->window;
+  a.nblk = (int32_t)(p->L / p->block_size);
+  a.L = (int32_t)p->L;
+  a.prefix = p->clean_prefix;
   a.scale = resolved_scale(p);
   a.scale_log2 = a.scale * 1.44269504088896340736f;
   a.out_f32 = (p->dtype == BDLM_F32 || p->out_f32) ? 1 : 0;
@@ -428,13 +440,24 @@ int64_t bdlm_visible_pairs(const bdlm_problem* p, int32_t n_q, const bdlm_range*
     if (check_range(p, q_ranges[i], "query", i) != BDLM_OK) return -1;
   for (int j = 0; j < n_k; ++j)
     if (check_range(p, k_ranges[j], "key", j) != BDLM_OK) return -1;
+  // A clean-context table lives in device memory: read it back (synchronously)
+  // and check its contract, which the asynchronous calls cannot.
+  std::vector<int> table;
+  if (p->clean_prefix) {
+    table.resize((size_t)(p->L / p->block_size));
+    if (hipMemcpy(table.data(), p->clean_prefix, table.size() * sizeof(int), hipMemcpyDeviceToHost) != hipSuccess)
+      return -1;
+    for (size_t b = 0; b < table.size(); ++b)
+      if (table[b] < 0 || table[b] > p->L || (b > 0 && table[b] < table[b - 1])) return -1;
+  }
+  const MaskRule rule = host_rule(p, p->clean_prefix ? table.data() : nullptr);
   int64_t tot = 0;
   for (int i = 0; i < n_q; ++i)
     for (int64_t r = 0; r < q_ranges[i].len; ++r) {
       const int pq = (int)(q_ranges[i].pos0 + r);
       for (int j = 0; j < n_k; ++j) {
         int lo, hi;
-        key_interval(q_ranges[i].stream, pq, k_ranges[j].stream, (int)p->block_size, p->clean_intra, lo, hi);
+        key_interval(q_ranges[i].stream, pq, k_ranges[j].stream, rule, lo, hi);
         lo = imax(lo, (int)k_ranges[j].pos0);
         hi = imin(hi, (int)(k_ranges[j].pos0 + k_ranges[j].len));
         if (hi > lo) tot += hi - lo;

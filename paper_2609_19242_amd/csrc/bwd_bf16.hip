@@ -161,8 +161,8 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
     sp.lb = (w == 2 ? qr.l2 : qr.delta) + lrow;
     sp.lrec = (uint32_t)(((int64_t)a.batch * H * qr.len - lrow) * 4);
     int lo0, hi0, lo1, hi1;
-    query_interval(qr.stream, kr.stream, kpos_first, a.M, a.intra, lo0, hi0);
-    query_interval(qr.stream, kr.stream, kpos_last, a.M, a.intra, lo1, hi1);
+    query_interval(qr.stream, kr.stream, kpos_first, rule_of(a), lo0, hi0);
+    query_interval(qr.stream, kr.stream, kpos_last, rule_of(a), lo1, hi1);
     const int u0 = imax(lo0 - qr.pos0, 0), u1 = imin(hi1 - qr.pos0, qr.len);
     if (u1 > u0) {
       sp.s0 = u0 / BM;
@@ -174,7 +174,7 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
       }
     }
     int lo, hi;
-    query_interval(qr.stream, kr.stream, pk, a.M, a.intra, lo, hi);
+    query_interval(qr.stream, kr.stream, pk, rule_of(a), lo, hi);
     lo = imax(lo, qr.pos0);
     hi = imin(hi, qr.pos0 + qr.len);
     sp.qa = lo;

@@ -47,7 +47,7 @@ __global__ __launch_bounds__(128) void bwd_dq_f32_kernel(const AttnArgs a) {
     for (int j = 0; j < a.n_k; ++j) {
       const KRangeArg& kr = a.kr[j];
       int lo, hi;
-      key_interval(qr.stream, pq, kr.stream, a.M, a.intra, lo, hi);
+      key_interval(qr.stream, pq, kr.stream, rule_of(a), lo, hi);
       lo = imax(lo, kr.pos0);
       hi = imin(hi, kr.pos0 + kr.len);
       for (int kp = lo; kp < hi; ++kp) {
@@ -103,7 +103,7 @@ __global__ __launch_bounds__(128) void bwd_dkv_f32_kernel(const AttnArgs a) {
     for (int i = 0; i < a.n_q; ++i) {
       const QRangeArg& qr = a.qr[i];
       int lo, hi;
-      query_interval(qr.stream, kr.stream, pk, a.M, a.intra, lo, hi);
+      query_interval(qr.stream, kr.stream, pk, rule_of(a), lo, hi);
       lo = imax(lo, qr.pos0);
       hi = imin(hi, qr.pos0 + qr.len);
       for (int pq = lo; pq < hi; ++pq) {

@@ -25,30 +25,71 @@ constexpr int kMaxK = 32;
 constexpr int kMaxParts = 32;
 constexpr int kBig = 0x3fffffff;  // "to the end of the stream" (positions stay below 2^30)
 
+__host__ __device__ inline int imax(int a, int b) { return a > b ? a : b; }
+__host__ __device__ inline int imin(int a, int b) { return a < b ? a : b; }
+
+// The mask's parameters.  block_size M and the clean-to-clean reading come
+// from Sec. 3.2.  Two optional generalisations keep every visible set an
+// interval with non-decreasing ends:
+//  * window W > 0 (sliding-window layers, App. "Savings Breakdowns"): a query
+//    sees only the last W positions of its clean context, i.e. clean keys in
+//    [e - W, e) where e is the end of the context it would see without the
+//    window (q + 1, the end of q's block, or the start of q's corrupted block);
+//  * prefix (DFlash2 drafter attention, eq:dflash2-block-attention): the clean
+//    context of corrupted block b ends at prefix[b] (the block's anchor a_b)
+//    instead of at M b.  The table holds nblk = L / M entries, non-decreasing
+//    and in [0, L]; entries are clamped into [0, L] when read, so a table that
+//    breaks the contract changes the mask but never addresses out of bounds.
+struct MaskRule {
+  int M, intra, window, nblk, L;
+  const int* prefix;  // device (kernels) or host (host code) table, or null
+};
+
+// End of the clean context of corrupted block b.
+__host__ __device__ inline int clean_end_of_block(const MaskRule& r, int b) {
+  if (!r.prefix) return b * r.M;
+  const int v = r.prefix[imin(imax(b, 0), r.nblk - 1)];
+  return imin(imax(v, 0), r.L);
+}
+
+// First corrupted block whose clean context ends after position x (nblk if none).
+__host__ __device__ inline int first_block_ending_after(const MaskRule& r, int x) {
+  if (!r.prefix) return imin(x / r.M + 1, r.nblk);
+  int lo = 0, hi = r.nblk;  // invariant: the answer lies in [lo, hi]
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (clean_end_of_block(r, mid) > x) hi = mid;
+    else lo = mid + 1;
+  }
+  return lo;
+}
+
 // Visible key positions [lo, hi) for a query of stream qs at position pq,
-// over keys of stream ks (block size M).  Empty when hi <= lo.
-__host__ __device__ inline void key_interval(int qs, int pq, int ks, int M, int intra, int& lo, int& hi) {
-  const int bq = pq / M;
+// over keys of stream ks.  Empty when hi <= lo.
+__host__ __device__ inline void key_interval(int qs, int pq, int ks, const MaskRule& r, int& lo, int& hi) {
+  const int M = r.M, bq = pq / M;
   if (qs == kClean) {
     lo = 0;
-    hi = (ks == kClean) ? (intra == kIntraBlock ? (bq + 1) * M : pq + 1) : 0;
+    hi = (ks == kClean) ? (r.intra == kIntraBlock ? (bq + 1) * M : pq + 1) : 0;
   } else if (ks == kCorrupted) {  // own corrupted block, bidirectional
     lo = bq * M;
     hi = lo + M;
-  } else {  // clean prefix of the earlier blocks
+  } else {  // clean context of the block: the clean prefix of the earlier blocks
     lo = 0;
-    hi = bq * M;
+    hi = clean_end_of_block(r, bq);
   }
+  if (ks == kClean && r.window > 0) lo = imax(lo, hi - r.window);
 }
 
 // Query positions [lo, hi) of stream qs that see a key of stream ks at
 // position pk (the same rules read from the key side).
-__host__ __device__ inline void query_interval(int qs, int ks, int pk, int M, int intra, int& lo, int& hi) {
-  const int bk = pk / M;
+__host__ __device__ inline void query_interval(int qs, int ks, int pk, const MaskRule& r, int& lo, int& hi) {
+  const int M = r.M, bk = pk / M, W = r.window;
   if (qs == kClean) {
     if (ks == kClean) {
-      lo = (intra == kIntraBlock) ? bk * M : pk;
-      hi = kBig;
+      lo = (r.intra == kIntraBlock) ? bk * M : pk;
+      // with a window: e(q) <= pk + W, e(q) = q + 1 or the end of q's block
+      hi = W <= 0 ? kBig : (r.intra == kIntraBlock ? M * ((pk + W) / M) : pk + W);
     } else {
       lo = kBig;
       hi = kBig;
@@ -57,13 +98,12 @@ __host__ __device__ inline void query_interval(int qs, int ks, int pk, int M, in
     lo = bk * M;
     hi = lo + M;
   } else {
-    lo = (bk + 1) * M;
-    hi = kBig;
+    // blocks whose clean context [e - W, e) holds pk: e > pk and e <= pk + W
+    lo = first_block_ending_after(r, pk) * M;
+    hi = W <= 0 ? kBig : first_block_ending_after(r, pk + W) * M;
   }
 }
 
-__host__ __device__ inline int imax(int a, int b) { return a > b ? a : b; }
-__host__ __device__ inline int imin(int a, int b) { return a < b ? a : b; }
 
 // One query range as the kernels see it.  Pointers are to element 0 of the
 // range for batch element 0; row i of batch b is at row (b * bstride + i).
@@ -102,6 +142,11 @@ struct AttnArgs {
   int32_t n_q, n_k;
   int32_t batch, heads, kv_heads, group;
   int32_t M, intra;
+  int32_t window;      // clean keys per query at most (0: no limit)
+  int32_t nblk;        // blocks per stream, L / M
+  int32_t L;
+  int32_t pad_rule;
+  const int* prefix;   // clean context end per corrupted block (device), or null
   float scale;        // softmax scale
   float scale_log2;   // scale * log2(e): scores are kept in the base-2 domain
   int32_t total_tiles;   // flattened tiles (query tiles for fwd, key tiles for bwd)
@@ -123,6 +168,10 @@ struct MergeArgs {
   void* o;
   float* lse;
 };
+
+__host__ __device__ inline MaskRule rule_of(const AttnArgs& a) {
+  return MaskRule{a.M, a.intra, a.window, a.nblk, a.L, a.prefix};
+}
 
 // Blocks are dispatched round-robin over the 8 XCDs of an MI355X.  Remap the
 // hardware block id so that consecutive logical ids run on the same XCD (and

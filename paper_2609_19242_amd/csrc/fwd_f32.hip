@@ -40,7 +40,7 @@ __global__ __launch_bounds__(kFwdRowsF32) void fwd_f32_kernel(const AttnArgs a) 
   for (int j = 0; j < a.n_k; ++j) {
     const KRangeArg& kr = a.kr[j];
     int lo, hi;
-    key_interval(qr.stream, pq, kr.stream, a.M, a.intra, lo, hi);
+    key_interval(qr.stream, pq, kr.stream, rule_of(a), lo, hi);
     lo = imax(lo, kr.pos0);
     hi = imin(hi, kr.pos0 + kr.len);
     for (int kp = lo; kp < hi; ++kp) {

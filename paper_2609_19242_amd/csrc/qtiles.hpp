@@ -49,8 +49,8 @@ __device__ inline void key_tile_span(const AttnArgs& a, int j, int qs, int pq0, 
                                      int& t0, int& t1, int& f0, int& f1) {
   const KRangeArg& kr = a.kr[j];
   int lo0, hi0, lo1, hi1;
-  key_interval(qs, pq0, kr.stream, a.M, a.intra, lo0, hi0);
-  key_interval(qs, pq1, kr.stream, a.M, a.intra, lo1, hi1);
+  key_interval(qs, pq0, kr.stream, rule_of(a), lo0, hi0);
+  key_interval(qs, pq1, kr.stream, rule_of(a), lo1, hi1);
   const int u0 = imax(lo0 - kr.pos0, 0), u1 = imin(hi1 - kr.pos0, kr.len);
   t0 = t1 = f0 = f1 = 0;
   if (u1 <= u0) return;
@@ -85,7 +85,7 @@ __device__ inline bool find_key_tile(const AttnArgs& a, int jj, int qs, int pq0,
 __device__ inline void lane_key_interval(const AttnArgs& a, int j, int qs, int pq, int& lo, int& w) {
   const KRangeArg& kr = a.kr[j];
   int l, h;
-  key_interval(qs, pq, kr.stream, a.M, a.intra, l, h);
+  key_interval(qs, pq, kr.stream, rule_of(a), l, h);
   l = imax(l, kr.pos0);
   h = imin(h, kr.pos0 + kr.len);
   lo = l;

@@ -156,3 +156,25 @@ def test_visible_pairs_csbp_rank_with_clean_queries():
     clean = (last - first + 1) * (first + 1 + last + 1) // 2
     assert clean == 2281709568
     assert bd.visible_pairs(p, qr, kr) == 2281963520 + clean
+
+
+# ------------------------------------------------------ mask generalisations
+def test_invalid_window_and_prefix_rejected():
+    assert _fwd(_prob(window=-1)) == -1
+    assert "window" in bd.lib().bdlm_last_error().decode()
+    p = _prob()
+    p.clean_prefix = FAKE + 2  # misaligned table pointer; never dereferenced
+    assert _fwd(p) == -1
+    assert "clean_prefix" in bd.lib().bdlm_last_error().decode()
+
+
+@pytest.mark.parametrize("L,M,W", [(256, 16, 1), (256, 16, 40), (512, 32, 100), (128, 8, 10000)])
+@pytest.mark.parametrize("reading", [bd.CLEAN_INTRA_CAUSAL, bd.CLEAN_INTRA_BLOCK])
+def test_windowed_visible_pairs_match_oracle_popcount(L, M, W, reading):
+    p = bd.make_problem(1, L, M, 2, 1, 128, bd.BF16, clean_intra=reading, window=W)
+    qr = [Range(CORRUPTED, 0, L), Range(CLEAN, 0, L)]
+    kr = [Range(CLEAN, 0, L // 2), Range(CORRUPTED, 0, L), Range(CLEAN, L // 2, L - L // 2)]
+    want = oracle.count_visible_pairs([(CORRUPTED, 0, L), (CLEAN, 0, L)],
+                                      [(CLEAN, 0, L // 2), (CORRUPTED, 0, L), (CLEAN, L // 2, L - L // 2)],
+                                      M, reading, window=W)
+    assert bd.visible_pairs(p, qr, kr) == want
