@@ -19,6 +19,9 @@ Also reported on the same JSON line:
 * per-kernel averages of the step;
 * one 256K CSBP rank's share (17 partial forwards, a 17-way LSE merge and the
   backward over the 17 key ranges) with the merge kernel's HBM roofline;
+* the mask generalisations at full size (mask_ext): the 32K shape in a
+  1,024-position sliding-window layer, and a drafter share of 2,048 draft
+  blocks of 16 over 32K target features with sorted anchors;
 * cpu_baseline: the fp64 oracle timed on this host on a bounded sample of the
   same workload (evenly spaced query rows of one head, forward + backward).
 
@@ -226,6 +229,75 @@ def bench_csbp(torch, bd, synth, steps, warmup):
     return res
 
 
+def _timed_steps(torch, bd, step, steps, warmup):
+    """Warm up, then time ``steps`` calls of ``step`` with per-kernel HIP-event records."""
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    bd.timing_enable(True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    bd.timing_enable(False)
+    return e0.elapsed_time(e1) / steps, per_kernel(bd.timing_collect())
+
+
+def bench_ext(torch, bd, synth, steps, warmup):
+    """The mask generalisations at full size: the 32K shape in a sliding-window
+    layer (1,024 positions) and a DFlash2 drafter share (2,048 draft blocks of
+    16 over 32K target features).  Useful TFLOP/s on their own valid pairs."""
+    out = {}
+    w = synth.WORKLOADS["32k-w1024"]
+    q, k, v, do = synth.make_joint(w, device="cuda")
+    L, M = w.L, w.block_size
+    p = bd.make_problem(1, L, M, w.heads, w.kv_heads, w.head_dim, torch.bfloat16, window=w.window)
+    r = bd.joint_ranges(L)
+    pairs = bd.visible_pairs(p, r, r)
+    o, lse = torch.empty_like(q), torch.empty((1, w.heads, 2 * L), dtype=torch.float32, device="cuda")
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    ws = torch.empty(bd.attn_bwd_workspace_bytes(p, r), dtype=torch.uint8, device="cuda")
+
+    def step_w():
+        bd.joint_fwd(q, k, v, M, out=(o, lse), window=w.window)
+        bd.joint_bwd(q, k, v, o, lse, do, M, out=(dq, dk, dv), workspace=ws, window=w.window)
+
+    ms, kern = _timed_steps(torch, bd, step_w, steps, warmup)
+    fl = bd.useful_flops(pairs, w.heads, 1, w.head_dim)
+    out["window32k"] = {"workload": w.describe(), "ms_per_step": ms, "useful_tflops": fl["total"] / (ms * 1e-3) / 1e12,
+                        "pairs_per_head": pairs, "kernels": kern}
+    del q, k, v, do, o, lse, dq, dk, dv, ws
+    torch.cuda.empty_cache()
+
+    w = synth.WORKLOADS["drafter32k"]
+    q, kd, vd, kt, vt, do, anchors = synth.make_drafter(w, device="cuda")
+    nd = w.draft_blocks * w.block_size
+    p = bd.make_problem(1, w.L, w.block_size, w.heads, w.kv_heads, w.head_dim, torch.bfloat16, clean_prefix=anchors)
+    qr = [bd.Range(bd.CORRUPTED, 0, nd)]
+    kr = [bd.Range(bd.CORRUPTED, 0, nd), bd.Range(bd.CLEAN, 0, w.L)]
+    pairs = bd.visible_pairs(p, qr, kr)
+    o, lse = torch.empty_like(q), torch.empty((1, w.heads, nd), dtype=torch.float32, device="cuda")
+    dq = torch.empty_like(q)
+    dks = [torch.empty_like(kd), torch.empty_like(kt)]
+    dvs = [torch.empty_like(vd), torch.empty_like(vt)]
+    ws = torch.empty(bd.attn_bwd_workspace_bytes(p, qr), dtype=torch.uint8, device="cuda")
+
+    def step_d():
+        bd.attn_fwd(p, qr, [q], [o], [lse], kr, [kd, kt], [vd, vt])
+        bd.attn_bwd(p, qr, [q], [o], [lse], [do], [dq], kr, [kd, kt], [vd, vt], dks, dvs, ws)
+
+    ms, kern = _timed_steps(torch, bd, step_d, steps, warmup)
+    assert torch.isfinite(o).all() and torch.isfinite(dq).all()
+    fl = bd.useful_flops(pairs, w.heads, 1, w.head_dim)
+    out["drafter32k"] = {"workload": w.describe(), "ms_per_step": ms, "useful_tflops": fl["total"] / (ms * 1e-3) / 1e12,
+                         "pairs_per_head": pairs, "kernels": kern}
+    del q, kd, vd, kt, vt, do, anchors, o, lse, dq, dks, dvs, ws
+    torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(bd, synth, budget_s):
     """The fp64 oracle on the host: forward + backward of evenly spaced query rows of one head of the 32K workload."""
     import numpy as np
@@ -276,6 +348,9 @@ def main():
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-csbp", action="store_true")
+    ap.add_argument("--no-ext", action="store_true", help="skip the sliding-window and drafter legs")
+    ap.add_argument("--ext-only", action="store_true",
+                    help="run only the sliding-window and drafter legs and print their result")
     ap.add_argument("--csbp-only", action="store_true",
                     help="run only the 256K CSBP leg and print its result (for per-workload kernel profiles)")
     ap.add_argument("--pmc-pass", action="store_true",
@@ -305,6 +380,9 @@ def main():
         torch.cuda.synchronize()
         print("[bench] pmc pass done", flush=True)
         return
+    if args.ext_only:
+        print(json.dumps({"ext": bench_ext(torch, bd, synth, args.steps, args.warmup)}), flush=True)
+        return
     if args.csbp_only:
         res = bench_csbp(torch, bd, synth, args.steps, args.warmup)
         print(json.dumps({"csbp256k": res}), flush=True)
@@ -315,6 +393,10 @@ def main():
     if csbp:
         print(f"[bench] csbp256k: {csbp['ms_per_step']:.3f} ms/step; with clean-shard queries "
               f"{csbp['rank_operator']['ms_per_step']:.3f} ms/step", flush=True)
+    ext = None if args.no_ext else bench_ext(torch, bd, synth, max(2, args.steps // 2), 1)
+    if ext:
+        print("[bench] " + "; ".join(f"{n}: {r['ms_per_step']:.3f} ms/step, {r['useful_tflops']:.1f} useful TFLOP/s"
+                                     for n, r in ext.items()), flush=True)
     cpu = None if args.no_cpu_baseline else cpu_baseline(bd, synth, args.cpu_budget_s)
     w = main_res["workload"]
     line = {
@@ -339,6 +421,7 @@ def main():
         "kernels": main_res["kernels"],
         "cpu_baseline": cpu,
         "csbp256k": csbp,
+        "mask_ext": ext,
     }
     print(json.dumps(line), flush=True)
 

@@ -41,6 +41,11 @@ class Workload:
     global position ``local_pos0``; its keys are the same rows' corrupted K/V
     plus a clean prefix of ``clean_tokens`` rows held as ``n_shards`` equal
     shards (Sec. 4.3 and Alg. 1 of the paper).
+
+    ``kind == "drafter"``: DFlash2 drafter attention (App. "DFlash2 Drafter
+    Training Methodology"): ``draft_blocks`` draft blocks of ``block_size``
+    rows (the corrupted stream) attend to themselves and to the target
+    features (the clean stream, ``L`` rows) before their anchors.
     """
 
     index: int
@@ -59,6 +64,8 @@ class Workload:
     local_pos0: int = 0
     clean_tokens: int = 0
     n_shards: int = 0
+    window: int = 0        # sliding window over the clean context (0: none)
+    draft_blocks: int = 0  # kind "drafter": draft blocks of block_size rows over L target-feature rows
 
     @property
     def torch_dtype(self) -> torch.dtype:
@@ -66,16 +73,23 @@ class Workload:
 
     @property
     def q_rows(self) -> int:
-        return 2 * self.L if self.kind == "joint" else self.local_tokens
+        if self.kind == "joint":
+            return 2 * self.L
+        return self.draft_blocks * self.block_size if self.kind == "drafter" else self.local_tokens
 
     @property
     def shard_tokens(self) -> int:
         return self.clean_tokens // self.n_shards if self.n_shards else 0
 
     def describe(self) -> str:
+        win = f", window {self.window}" if self.window else ""
         if self.kind == "joint":
             return (f"batch {self.batch}, L={self.L} clean + {self.L} corrupted, block {self.block_size}, "
-                    f"{self.heads}/{self.kv_heads} heads, d={self.head_dim}, {self.dtype}")
+                    f"{self.heads}/{self.kv_heads} heads, d={self.head_dim}, {self.dtype}{win}")
+        if self.kind == "drafter":
+            return (f"drafter: {self.draft_blocks} draft blocks of {self.block_size} over {self.L} target-feature "
+                    f"rows, sorted uniform anchors, {self.heads}/{self.kv_heads} heads, d={self.head_dim}, "
+                    f"{self.dtype}{win}")
         return (f"CSBP rank: {self.local_tokens} corrupted rows at {self.local_pos0}, block {self.block_size}, "
                 f"clean prefix {self.clean_tokens} as {self.n_shards} shards, "
                 f"{self.heads}/{self.kv_heads} heads, d={self.head_dim}, {self.dtype}")
@@ -89,6 +103,10 @@ WORKLOADS: Dict[str, Workload] = {
                          local_tokens=16384, local_pos0=131072, clean_tokens=262144, n_shards=16),
     "128k": Workload(5, "128k", "joint", 1, 131072, 128, 64, 8, 128, "bf16",
                      amplified_key_fraction=0.01, amplified_key_factor=8.0),
+    # The 32K shape in a sliding-window layer (the paper's 1,024-position window).
+    "32k-w1024": Workload(6, "32k-w1024", "joint", 1, 32768, 64, 32, 8, 128, "bf16", window=1024),
+    # A drafter share: 2,048 draft blocks of 16 over 32K target features.
+    "drafter32k": Workload(7, "drafter32k", "drafter", 1, 32768, 16, 32, 8, 128, "bf16", draft_blocks=2048),
 }
 BY_INDEX = {w.index: w for w in WORKLOADS.values()}
 
@@ -173,3 +191,31 @@ def make_csbp_clean_queries(w: Workload, device: str = "cpu", dtype: Optional[to
     base = 1000 * w.index if seed_base is None else seed_base
     shape = (1, w.shard_tokens, w.heads, w.head_dim)
     return normal(shape, base + 5, dt, device), normal(shape, base + 6, dt, device)
+
+
+def draft_anchors(w: Workload, device: str = "cpu") -> torch.Tensor:
+    """Anchors of the draft blocks: ``draft_blocks`` positions drawn uniformly
+    from [1, L] (seed tensor 4), sorted; one int32 entry per block of the
+    L-row stream, the entries past the draft blocks set to L."""
+    assert w.kind == "drafter"
+    nblk = w.L // w.block_size
+    g = generator(1000 * w.index + 4, "cpu")
+    a = torch.sort(torch.randint(1, w.L + 1, (w.draft_blocks,), generator=g)).values
+    a = torch.cat([a, torch.full((nblk - w.draft_blocks,), w.L)]).to(torch.int32)
+    return a.to(device)
+
+
+def make_drafter(w: Workload, device: str = "cpu", dtype: Optional[torch.dtype] = None, need_do: bool = True):
+    """Drafter tensors: ``q, k_draft, v_draft, k_target, v_target, do`` and the anchor table."""
+    assert w.kind == "drafter"
+    dt = dtype or w.torch_dtype
+    base = 1000 * w.index
+    nd = w.draft_blocks * w.block_size
+    q = normal((1, nd, w.heads, w.head_dim), base + 0, dt, device)
+    kall = normal((1, nd + w.L, w.kv_heads, w.head_dim), base + 1, dt, device)
+    vall = normal((1, nd + w.L, w.kv_heads, w.head_dim), base + 2, dt, device)
+    kd, kt = kall[:, :nd].contiguous(), kall[:, nd:].contiguous()
+    vd, vt = vall[:, :nd].contiguous(), vall[:, nd:].contiguous()
+    del kall, vall
+    do = normal((1, nd, w.heads, w.head_dim), base + 3, dt, device) if need_do else None
+    return q, kd, vd, kt, vt, do, draft_anchors(w, device)
