@@ -89,20 +89,49 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_kernel(const AttnArgs a) {
     c.have = find_key_tile(a, c.j + 1, qr.stream, pq0, pq1, BN, c.j, c.t, c.t1, c.f0, c.f1);
     return c;
   };
-  // LDS-DMA copy of a tile into stage st (empty copies past the last tile, so
-  // every wave issues IPW per tile); rows past the range end read zeros.
   const int64_t HKV = a.kv_heads;
+  // The copy cursor runs two tiles ahead of the compute cursor and carries
+  // the source pointer of its tile (this wave's tensor, batch and KV head
+  // applied) and the rows left in its range, so that advancing inside a range
+  // is one pointer increment; both are recomputed only when the range changes.
+  struct CopyCur {
+    KCur c;
+    const bf16* src;
+    int rows_left;
+  };
+  const bool kwave = w < NW / 2;
+  auto copy_seek = [&](CopyCur cc) -> CopyCur {
+    if (cc.c.have) {
+      const KRangeArg& kr = a.kr[cc.c.j];
+      cc.src = (const bf16*)(kwave ? kr.k : kr.v) +
+               (((int64_t)it.b * kr.bstride + (int64_t)cc.c.t * BN) * HKV + kvh) * D;
+      cc.rows_left = kr.len - cc.c.t * BN;
+    }
+    return cc;
+  };
+  auto copy_next = [&](CopyCur cc) -> CopyCur {
+    if (!cc.c.have) return cc;
+    if (++cc.c.t < cc.c.t1) {
+      cc.src += (int64_t)BN * HKV * D;
+      cc.rows_left -= BN;
+      return cc;
+    }
+    cc.c.have = find_key_tile(a, cc.c.j + 1, qr.stream, pq0, pq1, BN, cc.c.j, cc.c.t, cc.c.t1, cc.c.f0, cc.c.f1);
+    return copy_seek(cc);
+  };
+  // LDS-DMA copy of the cursor's tile into stage st (empty copies past the
+  // last tile, so every wave issues IPW per tile); rows past the range end
+  // read zeros.
   uint32_t voff[IPW];
   const int cw = w % (NW / 2);
 #pragma unroll
   for (int i = 0; i < IPW; ++i) voff[i] = swz_src_offset<D>((cw * IPW + i) * 64 + lane, HKV * D);
-  auto copy_tile = [&](bf16* st, const KCur cc) __attribute__((always_inline)) {
-    const KRangeArg& kr = a.kr[cc.have ? cc.j : 0];
-    const int nrows = cc.have ? imin(BN, kr.len - cc.t * BN) : 0;
-    const int64_t eoff = (((int64_t)it.b * kr.bstride + (int64_t)cc.t * BN) * HKV + kvh) * D;
-    const uint32_t bytes = cc.have ? (uint32_t)(((int64_t)(nrows - 1) * HKV * D + D) * 2) : 0u;
-    const auto r = make_rsrc((const bf16*)(w < NW / 2 ? kr.k : kr.v) + (cc.have ? eoff : 0), bytes);
-    bf16* dst = st + (w < NW / 2 ? 0 : BN * D) + cw * IPW * 512;
+  const bf16* const any_src = (const bf16*)a.kr[0].k;
+  auto copy_tile = [&](bf16* st, const CopyCur& cc) __attribute__((always_inline)) {
+    const int nrows = cc.c.have ? imin(BN, cc.rows_left) : 0;
+    const uint32_t bytes = cc.c.have ? (uint32_t)(((nrows - 1) * (int)HKV * D + D) * 2) : 0u;
+    const auto r = make_rsrc(cc.c.have ? cc.src : any_src, bytes);
+    bf16* dst = st + (kwave ? 0 : BN * D) + cw * IPW * 512;
 #pragma unroll
     for (int i = 0; i < IPW; ++i) buf_to_lds<16>(r, dst + i * 512, voff[i], 0);
   };
@@ -113,14 +142,16 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_kernel(const AttnArgs a) {
   // Three LDS stages, copies two tiles ahead (as in the forward).
   KCur c0;
   c0.have = find_key_tile(a, 0, qr.stream, pq0, pq1, BN, c0.j, c0.t, c0.t1, c0.f0, c0.f1);
-  KCur c1 = next_tile(c0), c2 = next_tile(c1);
-  copy_tile(lds, c0);
-  copy_tile(lds + STAGE, c1);
+  CopyCur cp = copy_seek(CopyCur{c0, any_src, 0});
+  copy_tile(lds, cp);
+  cp = copy_next(cp);
+  copy_tile(lds + STAGE, cp);
+  cp = copy_next(cp);
   vm_wait_barrier<IPW>();
   int cur = 0;
   int lane_lo = 0, lane_w = 0, lane_j = -1;
   while (c0.have) {
-    copy_tile(lds + (cur == 0 ? 2 : cur - 1) * STAGE, c2);
+    copy_tile(lds + (cur == 0 ? 2 : cur - 1) * STAGE, cp);
     const int j = c0.j, t = c0.t, f0 = c0.f0, f1 = c0.f1;
     if (lane_j != j) {
       lane_key_interval(a, j, qr.stream, pq, lane_lo, lane_w);
@@ -186,9 +217,8 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_kernel(const AttnArgs a) {
 
     vm_wait_barrier<IPW>();
     cur = cur == 2 ? 0 : cur + 1;
-    c0 = c1;
-    c1 = c2;
-    c2 = next_tile(c2);
+    c0 = next_tile(c0);
+    cp = copy_next(cp);
   }
   // Copies still in flight target stages nobody reads; they must land before
   // the workgroup's LDS is released.
