@@ -105,17 +105,19 @@ def bench_32k(torch, bd, synth, steps, warmup):
         step()
     torch.cuda.synchronize()
     bd.timing_enable(True)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
     t0 = time.perf_counter()
-    e0.record()
-    for _ in range(steps):
+    ev[0].record()
+    for i in range(steps):
         step()
-    e1.record()
+        ev[i + 1].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     bd.timing_enable(False)
     kern = per_kernel(bd.timing_collect())
-    ms = e0.elapsed_time(e1) / steps
+    per_step = sorted(ev[i].elapsed_time(ev[i + 1]) for i in range(steps))
+    ms = ev[0].elapsed_time(ev[steps]) / steps
+    median_ms = per_step[steps // 2] if steps % 2 else 0.5 * (per_step[steps // 2 - 1] + per_step[steps // 2])
     assert torch.isfinite(o).all() and torch.isfinite(dq).all()
     # Algorithmic FLOP per valid pair of each kernel: forward 4d (Q K^T, P V);
     # dK/dV kernel 8d (Q K^T, dO V^T, P^T dO, dS^T Q); dQ kernel 6d (Q K^T and
@@ -131,7 +133,10 @@ def bench_32k(torch, bd, synth, steps, warmup):
     roof = {"bound": "mfma", "kernel": dom, "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": recorded_traffic(dom),
             "flop_per_launch": kern[dom]["flop_per_launch"], "avg_launch_ms": kern[dom]["avg_ms"]}
-    res = {"ms_per_step": ms, "wall_s": wall, "pairs_per_head": pairs, "flops": fl, "kernels": kern,
+    fwd_ms = kern["fwd_bf16"]["avg_ms"]
+    bwd_ms = sum(kern[k]["avg_ms"] for k in ("bwd_pre", "bwd_dkdv_bf16", "bwd_dq_bf16") if k in kern)
+    res = {"ms_per_step": ms, "median_ms_per_step": median_ms, "fwd_ms": fwd_ms, "bwd_ms": bwd_ms,
+           "wall_s": wall, "pairs_per_head": pairs, "flops": fl, "kernels": kern,
            "roofline": roof, "value": fl["total"] / (ms * 1e-3) / 1e12, "workload": w}
     del q, k, v, do, o, lse, dq, dk, dv, ws
     torch.cuda.empty_cache()
@@ -298,6 +303,39 @@ def bench_ext(torch, bd, synth, steps, warmup):
     return out
 
 
+def bench_configs(torch, bd, synth, steps, warmup):
+    """Step time of the other joint workloads (parity-test configurations, not
+    bench lines): 4k (batch 2, block 32) and 128k (block 128, 64/8 heads, 1% of
+    keys x8) with and without the two-term P/dS products it needs for parity."""
+    out = {}
+    for name, hilo in (("4k", False), ("128k", False), ("128k", True)):
+        w = synth.WORKLOADS[name]
+        q, k, v, do = synth.make_joint(w, device="cuda")
+        B, n, Hq, D = q.shape
+        L, M = w.L, w.block_size
+        p = bd.make_problem(B, L, M, Hq, w.kv_heads, D, torch.bfloat16, hilo=hilo)
+        r = bd.joint_ranges(L)
+        pairs = bd.visible_pairs(p, r, r)
+        o, lse = torch.empty_like(q), torch.empty((B, Hq, n), dtype=torch.float32, device="cuda")
+        dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+        ws = torch.empty(bd.attn_bwd_workspace_bytes(p, r), dtype=torch.uint8, device="cuda")
+
+        def step():
+            bd.joint_fwd(q, k, v, M, out=(o, lse), hilo=hilo)
+            bd.joint_bwd(q, k, v, o, lse, do, M, out=(dq, dk, dv), workspace=ws, hilo=hilo)
+
+        ms, kern = _timed_steps(torch, bd, step, steps, warmup)
+        fl = bd.useful_flops(pairs, Hq, B, D)
+        out[name + ("-hilo" if hilo else "")] = {
+            "workload": w.describe() + (", hilo" if hilo else ""), "ms_per_step": ms,
+            "useful_tflops": fl["total"] / (ms * 1e-3) / 1e12, "pairs_per_head": pairs, "kernels": kern}
+        print(f"[bench] {name}{' hilo' if hilo else ''}: {ms:.3f} ms/step, "
+              f"{out[name + ('-hilo' if hilo else '')]['useful_tflops']:.1f} useful TFLOP/s", flush=True)
+        del q, k, v, do, o, lse, dq, dk, dv, ws
+        torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(bd, synth, budget_s):
     """The fp64 oracle on the host: forward + backward of evenly spaced query rows of one head of the 32K workload."""
     import numpy as np
@@ -349,6 +387,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-csbp", action="store_true")
     ap.add_argument("--no-ext", action="store_true", help="skip the sliding-window and drafter legs")
+    ap.add_argument("--configs-only", action="store_true",
+                    help="time only the 4k and 128k joint workloads and print their result")
     ap.add_argument("--ext-only", action="store_true",
                     help="run only the sliding-window and drafter legs and print their result")
     ap.add_argument("--csbp-only", action="store_true",
@@ -379,6 +419,9 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         print("[bench] pmc pass done", flush=True)
+        return
+    if args.configs_only:
+        print(json.dumps({"configs": bench_configs(torch, bd, synth, args.steps, args.warmup)}), flush=True)
         return
     if args.ext_only:
         print(json.dumps({"ext": bench_ext(torch, bd, synth, args.steps, args.warmup)}), flush=True)
@@ -416,6 +459,13 @@ def main():
                    "heads": w.heads, "kv_heads": w.kv_heads, "head_dim": w.head_dim, "clean_intra": "causal",
                    "parallelism": "single GPU"},
         "mfma_util_useful": main_res["value"] / PEAK_BF16_TFLOPS,
+        "median_ms_per_step": main_res["median_ms_per_step"],
+        "fwd_ms": main_res["fwd_ms"],
+        "bwd_ms": main_res["bwd_ms"],
+        "fwd_useful_tflops": main_res["flops"]["fwd"] / (main_res["fwd_ms"] * 1e-3) / 1e12,
+        "bwd_useful_tflops": main_res["flops"]["bwd"] / (main_res["bwd_ms"] * 1e-3) / 1e12,
+        # the stricter convention: 12 d per valid pair (no S recompute in the backward)
+        "useful_tflops_12d": main_res["value"] * 12 / 14,
         "useful_flop_per_step": main_res["flops"]["total"],
         "roofline": main_res["roofline"],
         "kernels": main_res["kernels"],
