@@ -26,7 +26,8 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(const AttnArgs a) {
   const int64_t rh = g / CPR;  // (b * len + row) * H + h
   const int h = (int)(rh % H);
   const int64_t brow = rh / H;
-  const int64_t row = brow % qr.len, b = brow / qr.len;
+  const int64_t len = qr.len > 0 ? qr.len : 1;  // a range of no rows launches no thread with ok set
+  const int64_t row = brow % len, b = brow / len;
   const int64_t off = ((b * qr.bstride + row) * H + h) * D + chunk * 8;
   float s = 0.f;
   if (ok) {

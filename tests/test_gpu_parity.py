@@ -265,3 +265,65 @@ def test_multi_range_fwd_bwd(split, heads):
     assert_close(f"{split} dQ", torch.cat([t.cpu() for t in dqd], dim=1), dQ, torch.bfloat16)
     assert_close(f"{split} dK", torch.cat([t.cpu() for t in dkd], dim=1), dK, torch.bfloat16)
     assert_close(f"{split} dV", torch.cat([t.cpu() for t in dvd], dim=1), dV, torch.bfloat16)
+
+
+# ---------------------------------------------------------- degenerate calls
+def test_degenerate_ranges():
+    """Zero-length query and key ranges next to ordinary ones change nothing
+    (bit for bit); a key range no query sees gets dK = dV = 0 exactly; a call
+    whose only query range is empty writes nothing."""
+    L, M, Hq, Hkv, D = 256, 16, 4, 2, 128
+    q, k, v, do = joint_inputs(L, Hq, Hkv, D, torch.bfloat16, seed=61)
+    qd, kd, vd, dod = (t.to(DEV) for t in (q, k, v, do))
+    o_ref, lse_ref = bd.joint_fwd(qd, kd, vd, M, out_f32=True)
+    dq_ref, dk_ref, dv_ref = bd.joint_bwd(qd, kd, vd, o_ref, lse_ref, dod, M, out_f32=True)
+
+    p = bd.make_problem(1, L, M, Hq, Hkv, D, torch.bfloat16, out_f32=True)
+    half = lambda t, s: t[:, (L if s == CLEAN else 0):(L if s == CLEAN else 0) + L].contiguous()
+    dummy_q = torch.zeros((1, 1, Hq, D), dtype=torch.bfloat16, device=DEV)
+    dummy_kv = torch.zeros((1, 1, Hkv, D), dtype=torch.bfloat16, device=DEV)
+    # Same range order as the joint call (the order of ranges is the order of
+    # accumulation), with an empty range between the two.
+    QR = [Range(CORRUPTED, 0, L), Range(CLEAN, 100, 0), Range(CLEAN, 0, L)]
+    KR = [Range(CORRUPTED, 0, L), Range(CORRUPTED, 50, 0), Range(CLEAN, 0, L)]
+    qs = [half(qd, CORRUPTED), dummy_q, half(qd, CLEAN)]
+    dos = [half(dod, CORRUPTED), dummy_q, half(dod, CLEAN)]
+    ks = [half(kd, CORRUPTED), dummy_kv, half(kd, CLEAN)]
+    vs = [half(vd, CORRUPTED), dummy_kv, half(vd, CLEAN)]
+    os_ = [torch.empty(t.shape, dtype=torch.float32, device=DEV) for t in qs]
+    ls = [torch.empty((1, Hq, t.shape[1]), dtype=torch.float32, device=DEV) for t in qs]
+    bd.attn_fwd(p, QR, qs, os_, ls, KR, ks, vs)
+    dqs = [torch.empty(t.shape, dtype=torch.float32, device=DEV) for t in qs]
+    dks = [torch.empty(t.shape, dtype=torch.float32, device=DEV) for t in ks]
+    dvs = [torch.empty(t.shape, dtype=torch.float32, device=DEV) for t in vs]
+    ws = torch.empty(bd.attn_bwd_workspace_bytes(p, QR), dtype=torch.uint8, device=DEV)
+    bd.attn_bwd(p, QR, qs, os_, ls, dos, dqs, KR, ks, vs, dks, dvs, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(os_[0], o_ref[:, :L]) and torch.equal(os_[2], o_ref[:, L:])
+    assert torch.equal(ls[0], lse_ref[:, :, :L]) and torch.equal(ls[2], lse_ref[:, :, L:])
+    assert torch.equal(dqs[0], dq_ref[:, :L]) and torch.equal(dqs[2], dq_ref[:, L:])
+    assert torch.equal(dks[0], dk_ref[:, :L]) and torch.equal(dks[2], dk_ref[:, L:])
+    assert torch.equal(dvs[0], dv_ref[:, :L]) and torch.equal(dvs[2], dv_ref[:, L:])
+
+    # clean queries only: the corrupted key range is seen by no query
+    QR2 = [Range(CLEAN, 0, L)]
+    KR2 = [Range(CLEAN, 0, L), Range(CORRUPTED, 0, L)]  # ks[2], ks[0] below
+    o2 = torch.empty(qs[2].shape, dtype=torch.float32, device=DEV)
+    l2 = torch.empty((1, Hq, L), dtype=torch.float32, device=DEV)
+    bd.attn_fwd(p, QR2, [qs[2]], [o2], [l2], KR2, [ks[2], ks[0]], [vs[2], vs[0]])
+    dq2 = torch.empty(qs[2].shape, dtype=torch.float32, device=DEV)
+    dk2 = [torch.full(t.shape, 5.0, dtype=torch.float32, device=DEV) for t in (ks[2], ks[0])]
+    dv2 = [torch.full(t.shape, 5.0, dtype=torch.float32, device=DEV) for t in (vs[2], vs[0])]
+    ws2 = torch.empty(bd.attn_bwd_workspace_bytes(p, QR2), dtype=torch.uint8, device=DEV)
+    bd.attn_bwd(p, QR2, [qs[2]], [o2], [l2], [dos[2]], [dq2], KR2, [ks[2], ks[0]], [vs[2], vs[0]], dk2, dv2, ws2)
+    torch.cuda.synchronize()
+    assert (dk2[1] == 0).all() and (dv2[1] == 0).all()
+    O, LSE = oracle.fwd(q[:, L:], k[:, L:], v[:, L:], [(CLEAN, 0, L)], [(CLEAN, 0, L)], M)
+    assert_close("clean-only O", o2, O, torch.bfloat16)
+
+    # a call whose only query range is empty writes nothing
+    sentinel = torch.full((1, 1, Hq, D), 3.0, dtype=torch.float32, device=DEV)
+    lsent = torch.full((1, Hq, 1), 3.0, dtype=torch.float32, device=DEV)
+    bd.attn_fwd(p, [Range(CLEAN, 0, 0)], [dummy_q], [sentinel], [lsent], KR2, [ks[2], ks[0]], [vs[2], vs[0]])
+    torch.cuda.synchronize()
+    assert (sentinel == 3.0).all() and (lsent == 3.0).all()
