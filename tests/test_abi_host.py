@@ -178,3 +178,22 @@ def test_windowed_visible_pairs_match_oracle_popcount(L, M, W, reading):
                                       [(CLEAN, 0, L // 2), (CORRUPTED, 0, L), (CLEAN, L // 2, L - L // 2)],
                                       M, reading, window=W)
     assert bd.visible_pairs(p, qr, kr) == want
+
+
+# ---------------------------------------------------------------- size limits
+def test_size_limits_rejected_before_launch():
+    L = bd.lib()
+    # positions must stay below 2^30
+    assert _fwd(_prob(L=1 << 30, block_size=1 << 20)) == -1
+    assert "2^30" in L.bdlm_last_error().decode()
+    # a query range whose batch * len * heads exceeds 2^28 is rejected by the backward
+    n = 1 << 24  # 2^24 rows x 32 heads = 2^29
+    p = bd.make_problem(1, n, 64, 32, 8, 128, bd.BF16)
+    qr = [Range(CORRUPTED, 0, n)]
+    need = bd.attn_bwd_workspace_bytes(p, qr)
+    f = bd._parr([FAKE])
+    rc = L.bdlm_attn_bwd(ctypes.byref(p), 1, bd._rarr(qr), f, f, f, f, f, 1, bd._rarr([Range(CLEAN, 0, 64)]),
+                         f, f, f, f, FAKE, need, None)
+    assert rc == -2 and "2^28" in L.bdlm_last_error().decode()
+    # more query ranges than the kernel arguments hold
+    assert _fwd(_prob(), qr=[Range(CORRUPTED, 0, 8)] * 5) == -2
