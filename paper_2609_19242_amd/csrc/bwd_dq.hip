@@ -163,17 +163,35 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_kernel(const AttnArgs a) {
     const uint32_t zr = sb + yrow;
     f32x16 sacc[2], dpacc[2];
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
+    for (int u = 0; u < 2; ++u)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         sacc[u][i] = 0.f;
         dpacc[u][i] = 0.f;
       }
+    {
+      // K and V fragments are read LA steps ahead of their products (steps
+      // run over (u, s)); the scheduling fences keep the compiler from
+      // sinking each read down to the product that uses it.
+      constexpr int LA = 2, NS = 2 * KS;
+      bf16x8 kf[LA + 1], vf[LA + 1];
+      auto addr = [&](int n) { return (zr ^ (32u * (n % KS))) + (n / KS) * 32 * RB; };
 #pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        const uint32_t ad = (zr ^ (32u * s)) + u * 32 * RB;
-        sacc[u] = mfma32(lds_load16(ad), qf[s], sacc[u]);
-        dpacc[u] = mfma32(lds_load16(ad + TB), df[s], dpacc[u]);
+      for (int n = 0; n < LA; ++n) {
+        kf[n] = lds_load16(addr(n));
+        vf[n] = lds_load16(addr(n) + TB);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int n = 0; n < NS; ++n) {
+        if (n + LA < NS) {
+          kf[(n + LA) % (LA + 1)] = lds_load16(addr(n + LA));
+          vf[(n + LA) % (LA + 1)] = lds_load16(addr(n + LA) + TB);
+        }
+        const int u = n / KS, s = n % KS;
+        sacc[u] = mfma32(kf[n % (LA + 1)], qf[s], sacc[u]);
+        dpacc[u] = mfma32(vf[n % (LA + 1)], df[s], dpacc[u]);
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
 

@@ -161,11 +161,31 @@ __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
     const uint32_t zr = sb + yrow;
     f32x16 sacc[2];
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
+    for (int u = 0; u < 2; ++u)
 #pragma unroll
       for (int i = 0; i < 16; ++i) sacc[u][i] = 0.f;
+    {
+      // K fragments are read LA k-steps ahead of their products; the
+      // scheduling fences keep the compiler from sinking each read down to
+      // the product that uses it (which left every MFMA waiting on an LDS
+      // read issued one product earlier).
+      constexpr int LA = 3;
+      bf16x8 kf[LA + 1][2];
 #pragma unroll
-      for (int s = 0; s < KS; ++s) sacc[u] = mfma32(lds_load16((zr ^ (32u * s)) + u * 32 * RB), qf[s], sacc[u]);
+      for (int s = 0; s < LA; ++s)
+#pragma unroll
+        for (int u = 0; u < 2; ++u) kf[s][u] = lds_load16((zr ^ (32u * s)) + u * 32 * RB);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        if (s + LA < KS) {
+#pragma unroll
+          for (int u = 0; u < 2; ++u) kf[(s + LA) % (LA + 1)][u] = lds_load16((zr ^ (32u * (s + LA))) + u * 32 * RB);
+        }
+#pragma unroll
+        for (int u = 0; u < 2; ++u) sacc[u] = mfma32(kf[s % (LA + 1)][u], qf[s], sacc[u]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
 
     if (!(t >= f0 && t < f1)) {
