@@ -170,7 +170,8 @@ bdlm_status bdlm_attn_partial_fwd(const bdlm_problem* p,
  *   o_parts[j] : [batch][rows][heads][head_dim] in part_dtype
  *   lse_parts[j] : [batch][heads][rows] fp32
  *   o : [batch][rows][heads][head_dim] in out_dtype;  lse : [batch][heads][rows] fp32
- * o and lse may alias neither input.  1 <= n_parts <= BDLM_MAX_MERGE_PARTS.
+ * o and lse may alias neither input.  1 <= n_parts <= BDLM_MAX_MERGE_PARTS;
+ * batch * rows * heads < 2^31 (else BDLM_ERR_UNSUPPORTED, nothing launched).
  */
 bdlm_status bdlm_lse_merge(int64_t batch, int64_t rows, int32_t heads, int32_t head_dim,
                            int32_t n_parts, const void* const* o_parts,

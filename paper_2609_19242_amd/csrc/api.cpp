@@ -260,6 +260,10 @@ bdlm_status bdlm_lse_merge(int64_t batch, int64_t rows, int32_t heads, int32_t h
                 (long long)rows, heads);
   if (head_dim != 64 && head_dim != 128)
     return fail(BDLM_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", head_dim);
+  constexpr int64_t kMaxUnits = ((int64_t)1 << 31) - 1;  // (row, head) pairs: the grid stays below 2^31 workgroups
+  if (rows > 0 && (batch > kMaxUnits / rows || (int64_t)heads > kMaxUnits / (batch * rows)))
+    return fail(BDLM_ERR_UNSUPPORTED, "merge of batch=%lld x rows=%lld x heads=%d exceeds 2^31 (row, head) pairs",
+                (long long)batch, (long long)rows, heads);
   if (n_parts < 1) return fail(BDLM_ERR_INVALID, "n_parts must be >= 1");
   if (n_parts > kMaxParts) return fail(BDLM_ERR_UNSUPPORTED, "n_parts=%d exceeds %d", n_parts, kMaxParts);
   if ((part_dtype != BDLM_BF16 && part_dtype != BDLM_F32) || (out_dtype != BDLM_BF16 && out_dtype != BDLM_F32))

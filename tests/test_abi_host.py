@@ -10,6 +10,7 @@ import os
 import re
 
 import pytest
+import torch
 
 import oracle
 import paper_2609_19242_amd as bd
@@ -43,6 +44,11 @@ def _prob(**kw):
 
 
 FAKE = 0x10000  # never dereferenced: these calls fail validation first
+# Tests that pass unmapped pointers run only where no GPU is visible: should a
+# validation bug let such a call through, nothing is launched on a device.
+# (Counting devices does not initialise the HIP runtime.)
+host_only = pytest.mark.skipif(torch.cuda.device_count() > 0,
+                               reason="passes unmapped pointers that validation must reject; host-only test")
 
 
 def _fwd(p, qr=None, kr=None, ptr=FAKE):
@@ -61,11 +67,13 @@ def _fwd(p, qr=None, kr=None, ptr=FAKE):
     (dict(batch=0), -1, "batch"),
     (dict(clean_intra=5), -1, "clean_intra"),
 ])
+@host_only
 def test_invalid_problem_rejected(kw, status, needle):
     assert _fwd(_prob(**kw)) == status
     assert needle in bd.lib().bdlm_last_error().decode()
 
 
+@host_only
 def test_invalid_ranges_rejected():
     p = _prob()
     assert _fwd(p, qr=[Range(CORRUPTED, 60, 8)]) == -1  # past L
@@ -81,6 +89,7 @@ def test_invalid_ranges_rejected():
                            None, None, None) == -1
 
 
+@host_only
 def test_merge_and_bwd_validation():
     L = bd.lib()
     parts = bd._parr([FAKE])
@@ -159,6 +168,7 @@ def test_visible_pairs_csbp_rank_with_clean_queries():
 
 
 # ------------------------------------------------------ mask generalisations
+@host_only
 def test_invalid_window_and_prefix_rejected():
     assert _fwd(_prob(window=-1)) == -1
     assert "window" in bd.lib().bdlm_last_error().decode()
@@ -181,6 +191,7 @@ def test_windowed_visible_pairs_match_oracle_popcount(L, M, W, reading):
 
 
 # ---------------------------------------------------------------- size limits
+@host_only
 def test_size_limits_rejected_before_launch():
     L = bd.lib()
     # positions must stay below 2^30
@@ -197,3 +208,8 @@ def test_size_limits_rejected_before_launch():
     assert rc == -2 and "2^28" in L.bdlm_last_error().decode()
     # more query ranges than the kernel arguments hold
     assert _fwd(_prob(), qr=[Range(CORRUPTED, 0, 8)] * 5) == -2
+    # a merge over 2^31 (row, head) pairs or more (the product is checked without overflowing)
+    parts = bd._parr([FAKE])
+    assert L.bdlm_lse_merge(1, 1 << 26, 32, 128, 1, parts, parts, 0, FAKE + 4096, FAKE + 8192, 0, None) == -2
+    assert "2^31" in L.bdlm_last_error().decode()
+    assert L.bdlm_lse_merge(1 << 40, 1 << 40, 1 << 30, 128, 1, parts, parts, 0, FAKE + 4096, FAKE + 8192, 0, None) == -2
