@@ -327,3 +327,52 @@ def test_degenerate_ranges():
     bd.attn_fwd(p, [Range(CLEAN, 0, 0)], [dummy_q], [sentinel], [lsent], KR2, [ks[2], ks[0]], [vs[2], vs[0]])
     torch.cuda.synchronize()
     assert (sentinel == 3.0).all() and (lsent == 3.0).all()
+
+
+# ------------------------------------------ strided ranges, poisoned padding
+def test_strided_ranges_poisoned_padding():
+    """Ranges stored with batch_stride > len (batch 2) whose padding rows hold
+    NaN in every input: results match the oracle on the dense data (no padding
+    row is ever used), and the padding rows of every output (O, LSE, dQ, dK,
+    dV) keep their sentinel (nothing is written outside a range)."""
+    L, M, Hq, Hkv, D, B = 300, 12, 4, 2, 128, 2
+    SQ, SK = L + 37, L + 21  # row strides of the query-side and key-side tensors
+    q, k, v, do = joint_inputs(L, Hq, Hkv, D, torch.bfloat16, batch=B, seed=71)
+    streams = (CORRUPTED, CLEAN)
+
+    def strided(t, s, stride, fill):  # one stream's rows of a joint tensor, padded to `stride` rows
+        out = torch.full((B, stride) + tuple(t.shape[2:]), fill, dtype=t.dtype)
+        out[:, :L] = t[:, (L if s == CLEAN else 0):(L if s == CLEAN else 0) + L]
+        return out.to(DEV)
+
+    nan = float("nan")
+    QR = [Range(s, 0, L, SQ) for s in streams]
+    KR = [Range(s, 0, L, SK) for s in streams]
+    qs = [strided(q, s, SQ, nan) for s in streams]
+    dos = [strided(do, s, SQ, nan) for s in streams]
+    ks = [strided(k, s, SK, nan) for s in streams]
+    vs = [strided(v, s, SK, nan) for s in streams]
+    SENT = 7.0
+    os_ = [torch.full((B, SQ, Hq, D), SENT, dtype=torch.float32, device=DEV) for _ in streams]
+    ls = [torch.full((B, Hq, SQ), SENT, dtype=torch.float32, device=DEV) for _ in streams]
+    p = bd.make_problem(B, L, M, Hq, Hkv, D, torch.bfloat16, out_f32=True)
+    bd.attn_fwd(p, QR, qs, os_, ls, KR, ks, vs)
+    dqs = [torch.full((B, SQ, Hq, D), SENT, dtype=torch.float32, device=DEV) for _ in streams]
+    dks = [torch.full((B, SK, Hkv, D), SENT, dtype=torch.float32, device=DEV) for _ in streams]
+    dvs = [torch.full((B, SK, Hkv, D), SENT, dtype=torch.float32, device=DEV) for _ in streams]
+    ws = torch.empty(bd.attn_bwd_workspace_bytes(p, QR), dtype=torch.uint8, device=DEV)
+    bd.attn_bwd(p, QR, qs, os_, ls, dos, dqs, KR, ks, vs, dks, dvs, ws)
+    torch.cuda.synchronize()
+
+    for t in os_ + dqs + dks + dvs:
+        assert (t[:, L:] == SENT).all(), "a padding row was written"
+    for t in ls:
+        assert (t[:, :, L:] == SENT).all(), "a padding LSE entry was written"
+    joint = lambda ts: torch.cat([t[:, :L].cpu() for t in ts], dim=1)
+    O, LSE = oracle.joint_fwd(q, k, v, L, M)
+    dQ, dK, dV = oracle.joint_bwd(q, k, v, O, LSE, do, L, M)
+    assert_close("strided O", joint(os_), O, torch.bfloat16)
+    assert_close("strided LSE", torch.cat([t[:, :, :L].cpu() for t in ls], dim=2), LSE, torch.bfloat16)
+    assert_close("strided dQ", joint(dqs), dQ, torch.bfloat16)
+    assert_close("strided dK", joint(dks), dK, torch.bfloat16)
+    assert_close("strided dV", joint(dvs), dV, torch.bfloat16)
