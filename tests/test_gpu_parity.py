@@ -330,14 +330,16 @@ def test_degenerate_ranges():
 
 
 # ------------------------------------------ strided ranges, poisoned padding
-def test_strided_ranges_poisoned_padding():
+@pytest.mark.parametrize("dt", ["bf16", "fp32"])
+def test_strided_ranges_poisoned_padding(dt):
     """Ranges stored with batch_stride > len (batch 2) whose padding rows hold
     NaN in every input: results match the oracle on the dense data (no padding
     row is ever used), and the padding rows of every output (O, LSE, dQ, dK,
     dV) keep their sentinel (nothing is written outside a range)."""
     L, M, Hq, Hkv, D, B = 300, 12, 4, 2, 128, 2
     SQ, SK = L + 37, L + 21  # row strides of the query-side and key-side tensors
-    q, k, v, do = joint_inputs(L, Hq, Hkv, D, torch.bfloat16, batch=B, seed=71)
+    dtype = torch.float32 if dt == "fp32" else torch.bfloat16
+    q, k, v, do = joint_inputs(L, Hq, Hkv, D, dtype, batch=B, seed=71)
     streams = (CORRUPTED, CLEAN)
 
     def strided(t, s, stride, fill):  # one stream's rows of a joint tensor, padded to `stride` rows
@@ -355,7 +357,7 @@ def test_strided_ranges_poisoned_padding():
     SENT = 7.0
     os_ = [torch.full((B, SQ, Hq, D), SENT, dtype=torch.float32, device=DEV) for _ in streams]
     ls = [torch.full((B, Hq, SQ), SENT, dtype=torch.float32, device=DEV) for _ in streams]
-    p = bd.make_problem(B, L, M, Hq, Hkv, D, torch.bfloat16, out_f32=True)
+    p = bd.make_problem(B, L, M, Hq, Hkv, D, dtype, out_f32=True)
     bd.attn_fwd(p, QR, qs, os_, ls, KR, ks, vs)
     dqs = [torch.full((B, SQ, Hq, D), SENT, dtype=torch.float32, device=DEV) for _ in streams]
     dks = [torch.full((B, SK, Hkv, D), SENT, dtype=torch.float32, device=DEV) for _ in streams]
@@ -371,8 +373,8 @@ def test_strided_ranges_poisoned_padding():
     joint = lambda ts: torch.cat([t[:, :L].cpu() for t in ts], dim=1)
     O, LSE = oracle.joint_fwd(q, k, v, L, M)
     dQ, dK, dV = oracle.joint_bwd(q, k, v, O, LSE, do, L, M)
-    assert_close("strided O", joint(os_), O, torch.bfloat16)
-    assert_close("strided LSE", torch.cat([t[:, :, :L].cpu() for t in ls], dim=2), LSE, torch.bfloat16)
-    assert_close("strided dQ", joint(dqs), dQ, torch.bfloat16)
-    assert_close("strided dK", joint(dks), dK, torch.bfloat16)
-    assert_close("strided dV", joint(dvs), dV, torch.bfloat16)
+    assert_close(f"{dt} strided O", joint(os_), O, dtype)
+    assert_close(f"{dt} strided LSE", torch.cat([t[:, :, :L].cpu() for t in ls], dim=2), LSE, dtype)
+    assert_close(f"{dt} strided dQ", joint(dqs), dQ, dtype)
+    assert_close(f"{dt} strided dK", joint(dks), dK, dtype)
+    assert_close(f"{dt} strided dV", joint(dvs), dV, dtype)
