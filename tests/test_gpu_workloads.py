@@ -1,4 +1,5 @@
-"""GPU parity at the full workload sizes (32K joint, one 256K CSBP rank, 128K joint).
+"""GPU parity at the full workload sizes (32K joint, one 256K CSBP rank, 128K joint, and the
+32K sliding-window and drafter legs of the mask generalisations).
 
 The GPU computes every head and row in the launch configuration bench.py
 times.  The fp64 oracle checks, on the query heads of KV groups {0, last}:
@@ -52,12 +53,12 @@ def dv_identity(dv, do, group, tag):
     assert err < 5e-3, err
 
 
-def joint_check(w, reading=0, n_random=24, hilo=False):
+def joint_check(w, reading=0, n_random=24, hilo=False, window=0):
     L, M = w.L, w.block_size
     torch.cuda.empty_cache()
     q, k, v, do = synth.make_joint(w, device=DEV)
-    o, lse = bd.joint_fwd(q, k, v, M, clean_intra=reading, out_f32=True, hilo=hilo)
-    dq, dk, dv = bd.joint_bwd(q, k, v, o, lse, do, M, clean_intra=reading, out_f32=True, hilo=hilo)
+    o, lse = bd.joint_fwd(q, k, v, M, clean_intra=reading, out_f32=True, hilo=hilo, window=window)
+    dq, dk, dv = bd.joint_bwd(q, k, v, o, lse, do, M, clean_intra=reading, out_f32=True, hilo=hilo, window=window)
     torch.cuda.synchronize()
     tag = w.name
     assert torch.isfinite(o).all() and torch.isfinite(lse).all()
@@ -76,13 +77,15 @@ def joint_check(w, reading=0, n_random=24, hilo=False):
     # ---- sampled query rows: O, LSE, dQ
     rows = sample_rows(L, M, n_random, seed=w.index)
     single = [(int(s_all[i]), int(p_all[i]), 1) for i in rows]
-    O, LSE = oracle.fwd(qc[:, rows], kc, vc, single, r, M, clean_intra=reading, chunk=128)
+    O, LSE = oracle.fwd(qc[:, rows], kc, vc, single, r, M, clean_intra=reading, chunk=128, window=window)
     assert_close(f"{tag} O rows", o[:, rows][:, :, hs], O, BF16)
     assert_close(f"{tag} LSE rows", lse[:, hs][:, :, rows], LSE, BF16)
-    dQ, _, _ = oracle.bwd(qc[:, rows], kc, vc, O, LSE, doc[:, rows], single, r, M, clean_intra=reading, chunk=128)
+    dQ, _, _ = oracle.bwd(qc[:, rows], kc, vc, O, LSE, doc[:, rows], single, r, M, clean_intra=reading, chunk=128,
+                          window=window)
     assert_close(f"{tag} dQ rows", dq[:, rows][:, :, hs], dQ, BF16)
 
     # ---- key rows with few visible queries: corrupted blocks and the last two clean blocks
+    # (with a window of at least 2M positions the same query rows are all that see them)
     nb = L // M
     key_sets = []
     for blk in (0, 1, nb // 2, nb - 1):
@@ -92,9 +95,9 @@ def joint_check(w, reading=0, n_random=24, hilo=False):
     key_sets.append(("last clean blocks", qrows, list(range(2 * L - 2 * M, 2 * L))))
     for name, qrows, krows in key_sets:
         single = [(int(s_all[i]), int(p_all[i]), 1) for i in qrows]
-        Oq, Lq = oracle.fwd(qc[:, qrows], kc, vc, single, r, M, clean_intra=reading, chunk=128)
+        Oq, Lq = oracle.fwd(qc[:, qrows], kc, vc, single, r, M, clean_intra=reading, chunk=128, window=window)
         _, dK, dV = oracle.bwd(qc[:, qrows], kc, vc, Oq, Lq, doc[:, qrows], single, r, M, clean_intra=reading,
-                               chunk=128)
+                               chunk=128, window=window)
         assert_close(f"{tag} dK {name}", dk[:, krows][:, :, kvs], dK[:, krows], BF16)
         assert_close(f"{tag} dV {name}", dv[:, krows][:, :, kvs], dV[:, krows], BF16)
     del q, k, v, do, o, lse, dq, dk, dv
@@ -107,6 +110,77 @@ def test_workload_32k_causal():
 
 def test_workload_32k_block_reading():
     joint_check(WORKLOADS["32k"], 1, n_random=8)
+
+
+def test_workload_32k_window_1024():
+    """The 32K shape in a sliding-window layer (1,024 positions), as bench.py times it."""
+    w = WORKLOADS["32k-w1024"]
+    assert w.window >= 2 * w.block_size
+    joint_check(w, 0, n_random=16, window=w.window)
+
+
+def test_workload_drafter32k():
+    """The drafter share as bench.py times it: 2,048 draft blocks of 16 over 32,768
+    target-feature rows.  Sampled draft rows (O, LSE, dQ); the draft keys of
+    sampled blocks (seen by their own block only) and the last 64 target rows
+    (seen only by the blocks whose anchors pass them): dK, dV complete; the
+    sum-dV identity over both key ranges."""
+    w = WORKLOADS["drafter32k"]
+    torch.cuda.empty_cache()
+    q, kd, vd, kt, vt, do, anchors = synth.make_drafter(w, device=DEV)
+    M, T = w.block_size, w.L
+    nd = w.draft_blocks * M
+    p = bd.make_problem(1, T, M, w.heads, w.kv_heads, w.head_dim, torch.bfloat16, out_f32=True, clean_prefix=anchors)
+    qr = [Range(CORRUPTED, 0, nd)]
+    kr = [Range(CORRUPTED, 0, nd), Range(CLEAN, 0, T)]
+    o = torch.empty(q.shape, dtype=F32, device=DEV)
+    lse = torch.empty((1, w.heads, nd), dtype=F32, device=DEV)
+    bd.attn_fwd(p, qr, [q], [o], [lse], kr, [kd, kt], [vd, vt])
+    dq = torch.empty(q.shape, dtype=F32, device=DEV)
+    dks = [torch.empty(t.shape, dtype=F32, device=DEV) for t in (kd, kt)]
+    dvs = [torch.empty(t.shape, dtype=F32, device=DEV) for t in (vd, vt)]
+    ws = torch.empty(bd.attn_bwd_workspace_bytes(p, qr), dtype=torch.uint8, device=DEV)
+    bd.attn_bwd(p, qr, [q], [o], [lse], [do], [dq], kr, [kd, kt], [vd, vt], dks, dvs, ws)
+    torch.cuda.synchronize()
+    tag = w.name
+    assert torch.isfinite(o).all() and torch.isfinite(dq).all()
+    dv_identity(torch.cat(dvs, dim=1), do, w.heads // w.kv_heads, tag)
+
+    kvs = [0, w.kv_heads - 1]
+    hs = kv_group_heads(w.heads, w.kv_heads, kvs)
+    qc, doc = to_cpu_heads(q, hs), to_cpu_heads(do, hs)
+    kc = torch.cat([kd[:, :, kvs], kt[:, :, kvs]], dim=1).cpu()
+    vc = torch.cat([vd[:, :, kvs], vt[:, :, kvs]], dim=1).cpu()
+    pl = anchors.cpu().tolist()
+    okr = [(CORRUPTED, 0, nd), (CLEAN, 0, T)]
+
+    rows = sorted(set([0, M - 1, M, nd // 2, nd - M, nd - 1] +
+                      np.random.default_rng(w.index).choice(nd, size=16, replace=False).tolist()))
+    single = [(CORRUPTED, int(i), 1) for i in rows]
+    O, LSE = oracle.fwd(qc[:, rows], kc, vc, single, okr, M, chunk=128, clean_prefix=pl)
+    assert_close(f"{tag} O rows", o[:, rows][:, :, hs], O, BF16)
+    assert_close(f"{tag} LSE rows", lse[:, hs][:, :, rows], LSE, BF16)
+    dQ, _, _ = oracle.bwd(qc[:, rows], kc, vc, O, LSE, doc[:, rows], single, okr, M, chunk=128, clean_prefix=pl)
+    assert_close(f"{tag} dQ rows", dq[:, rows][:, :, hs], dQ, BF16)
+
+    nb = w.draft_blocks
+    last = list(range(T - 64, T))
+    seers = [b for b in range(nb) if pl[b] > T - 64]  # blocks whose target context reaches the last 64 rows
+    key_sets = [(f"draft block {b}", list(range(b * M, (b + 1) * M)), 0, list(range(b * M, (b + 1) * M)))
+                for b in (0, 1, nb // 2, nb - 1)]
+    key_sets.append(("last target rows", [i for b in seers for i in range(b * M, (b + 1) * M)], 1, last))
+    for name, qrows, kidx, krows in key_sets:
+        assert qrows, name
+        single = [(CORRUPTED, int(i), 1) for i in qrows]
+        Oq, Lq = oracle.fwd(qc[:, qrows], kc, vc, single, okr, M, chunk=128, clean_prefix=pl)
+        _, dK, dV = oracle.bwd(qc[:, qrows], kc, vc, Oq, Lq, doc[:, qrows], single, okr, M, chunk=128,
+                               clean_prefix=pl)
+        off = 0 if kidx == 0 else nd
+        kk = [off + x for x in krows]
+        assert_close(f"{tag} dK {name}", dks[kidx][:, krows][:, :, kvs], dK[:, kk], BF16)
+        assert_close(f"{tag} dV {name}", dvs[kidx][:, krows][:, :, kvs], dV[:, kk], BF16)
+    del q, kd, vd, kt, vt, do, o, lse, dq, dks, dvs, ws
+    torch.cuda.empty_cache()
 
 
 def test_workload_128k():
