@@ -378,3 +378,37 @@ def test_strided_ranges_poisoned_padding(dt):
     assert_close(f"{dt} strided dQ", joint(dqs), dQ, dtype)
     assert_close(f"{dt} strided dK", joint(dks), dK, dtype)
     assert_close(f"{dt} strided dV", joint(dvs), dV, dtype)
+
+
+# ------------------------------------------------------------- side stream
+def test_calls_run_on_the_given_stream():
+    """Every entry point enqueues on the stream it is given: a forward and
+    backward on a side stream (default priority), synchronised through that
+    stream alone, equal the same calls on the current stream bit for bit, and
+    the timing hooks record their kernels."""
+    L, M, Hq, Hkv, D = 320, 16, 4, 2, 128
+    q, k, v, do = joint_inputs(L, Hq, Hkv, D, torch.bfloat16, seed=83)
+    qd, kd, vd, dod = (t.to(DEV) for t in (q, k, v, do))
+    o_ref, lse_ref = bd.joint_fwd(qd, kd, vd, M, out_f32=True)
+    dq_ref, dk_ref, dv_ref = bd.joint_bwd(qd, kd, vd, o_ref, lse_ref, dod, M, out_f32=True)
+    torch.cuda.synchronize()
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        o = torch.empty(qd.shape, dtype=torch.float32, device=DEV)
+        lse = torch.empty(lse_ref.shape, dtype=torch.float32, device=DEV)
+        grads = tuple(torch.empty(t.shape, dtype=torch.float32, device=DEV) for t in (qd, kd, vd))
+        p = bd.make_problem(1, L, M, Hq, Hkv, D, torch.bfloat16)
+        ws = torch.empty(bd.attn_bwd_workspace_bytes(p, bd.joint_ranges(L)), dtype=torch.uint8, device=DEV)
+    bd.timing_enable(True)
+    bd.joint_fwd(qd, kd, vd, M, out_f32=True, out=(o, lse), stream=side)
+    bd.joint_bwd(qd, kd, vd, o, lse, dod, M, out_f32=True, out=grads, workspace=ws, stream=side)
+    side.synchronize()
+    recs = bd.timing_collect()
+    bd.timing_enable(False)
+    assert [n for n, _ in recs] == ["fwd_bf16", "bwd_pre", "bwd_dkdv_bf16", "bwd_dq_bf16"], recs
+    assert all(ms > 0 for _, ms in recs)
+    assert torch.equal(o, o_ref) and torch.equal(lse, lse_ref)
+    for a, b in zip(grads, (dq_ref, dk_ref, dv_ref)):
+        assert torch.equal(a, b)
