@@ -113,9 +113,9 @@ typedef struct {
                          matrix work of those products), for inputs with large scores or |dS|,
                          e.g. keys of large norm.  Ignored by the fp32 path. */
   int64_t window;     /* 0: no limit.  > 0: a query sees only the last `window` positions of its clean
-                         context (sliding-window layers; see "Mask generalisations" below) */
+                         context (sliding-window layers; see "Mask generalisations" above) */
   const int32_t* clean_prefix; /* NULL, or a device array of L / block_size ints: the end of the clean
-                         context of corrupted block b (DFlash2 anchors; see below).  Read by the kernels
+                         context of corrupted block b (DFlash2 anchors; see above).  Read by the kernels
                          during the call's execution; bdlm_visible_pairs reads it synchronously. */
 } bdlm_problem;
 
