@@ -9,7 +9,6 @@ complementary views of the AR-to-BDLM objective as batch elements; and
 workload-sized cases (a 1,024-position window at 4K, a drafter with 256
 draft blocks over 8,192 target features) on a subset of heads.
 """
-import numpy as np
 import pytest
 import torch
 

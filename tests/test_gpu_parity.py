@@ -6,7 +6,6 @@ backward key tiles, 32-row backward query steps); they cover both readings of
 the clean-to-clean rule, GQA groups, head_dim 64 and 128, batch > 1, the
 degenerate block sizes (1 and L) and rows that see no key.
 """
-import numpy as np
 import pytest
 import torch
 

@@ -7,7 +7,6 @@ on special cases, closed-form pair counts (App. B), or an invariant the paper
 proves (per-block separability, exact LSE merge of partials, the clean-gradient
 sum of eq. ``eq:correctness-clean-gradient``).
 """
-import itertools
 import math
 import os
 
