@@ -411,3 +411,15 @@ def test_calls_run_on_the_given_stream():
     assert torch.equal(o, o_ref) and torch.equal(lse, lse_ref)
     for a, b in zip(grads, (dq_ref, dk_ref, dv_ref)):
         assert torch.equal(a, b)
+
+
+# ------------------------------------------------------- head_dim 64, more tiles
+@pytest.mark.parametrize("reading", [0, 1], ids=["causal", "block"])
+def test_medium_head_dim_64(reading):
+    """head_dim 64 over many tiles: batch 2, L = 2,048 + 2,048, block 32, 16/4
+    heads (the d = 64 kernels otherwise meet only the small shapes); query
+    heads of KV groups {0, 3} against the oracle."""
+    L, M, Hq, Hkv, D, B = 2048, 32, 16, 4, 64, 2
+    q, k, v, do = joint_inputs(L, Hq, Hkv, D, torch.bfloat16, batch=B, seed=97 + reading)
+    check_joint(q, k, v, do, M, reading, torch.bfloat16, heads=kv_group_heads(Hq, Hkv, [0, Hkv - 1]),
+                tag=f"d64 L{L} r{reading}")
