@@ -6,6 +6,7 @@ backward key tiles, 32-row backward query steps); they cover both readings of
 the clean-to-clean rule, GQA groups, head_dim 64 and 128, batch > 1, the
 degenerate block sizes (1 and L) and rows that see no key.
 """
+import numpy as np
 import pytest
 import torch
 
@@ -423,3 +424,72 @@ def test_medium_head_dim_64(reading):
     q, k, v, do = joint_inputs(L, Hq, Hkv, D, torch.bfloat16, batch=B, seed=97 + reading)
     check_joint(q, k, v, do, M, reading, torch.bfloat16, heads=kv_group_heads(Hq, Hkv, [0, Hkv - 1]),
                 tag=f"d64 L{L} r{reading}")
+
+
+# ------------------------------------------------------- the call-size limits
+@pytest.mark.parametrize("D", [64, 128])
+def test_merge_max_parts(D):
+    """A merge of the maximum 32 partials (head_dim 64: per-lane LSE loads;
+    128: the two-register lane broadcast of parts 0-15 and 16-31), with empty
+    parts per row, bf16 and fp32 partials, against the oracle's merge."""
+    g = torch.Generator().manual_seed(5 + D)
+    B, R, H, J = 1, 45, 2, bd.MAX_MERGE_PARTS
+    os_ = [torch.randn(B, R, H, D, generator=g) for _ in range(J)]
+    ls = [torch.randn(B, H, R, generator=g) * 3 for _ in range(J)]
+    for j in range(J):
+        ls[j][torch.rand(B, H, R, generator=g) < 0.4] = -float("inf")
+    ls[J - 1][:, :, 7] = 9.0  # a row dominated by the last part
+    for j in range(J):
+        os_[j] = torch.where(torch.isneginf(ls[j]).transpose(1, 2)[..., None], torch.zeros(()), os_[j]).contiguous()
+    for pdt in (torch.float32, torch.bfloat16):
+        od = [t.to(pdt).to(DEV) for t in os_]
+        ld = [t.to(DEV) for t in ls]
+        o = torch.empty(B, R, H, D, dtype=torch.float32, device=DEV)
+        lse = torch.empty(B, H, R, dtype=torch.float32, device=DEV)
+        bd.lse_merge(od, ld, o, lse)
+        torch.cuda.synchronize()
+        Or, Lr = oracle.lse_merge([t.to(pdt) for t in os_], ls)
+        tol = torch.float32 if pdt == torch.float32 else torch.bfloat16
+        assert_close(f"merge J{J} d{D} {pdt} O", o, Or, tol)
+        assert_close(f"merge J{J} d{D} {pdt} LSE", lse, Lr, tol)
+
+
+def test_max_query_and_key_ranges():
+    """The largest call: 4 query ranges and 32 key ranges (the clean stream cut
+    into 31 uneven pieces, each its own tensor), forward and backward in one
+    call each, against the oracle over the same ranges."""
+    L, M, Hq, Hkv, D = 640, 16, 4, 2, 128
+    q, k, v, do = joint_inputs(L, Hq, Hkv, D, torch.bfloat16, seed=101)
+    cuts = sorted(set([0, L] + np.random.default_rng(7).choice(np.arange(1, L), size=30, replace=False).tolist()))
+    assert len(cuts) == 32
+    krs = [(CORRUPTED, 0, L)] + [(CLEAN, a, b - a) for a, b in zip(cuts[:-1], cuts[1:])]
+    qrs = [(CLEAN, 300, 340), (CORRUPTED, 0, 333), (CLEAN, 0, 300), (CORRUPTED, 333, 307)]
+    assert len(krs) == bd.MAX_K_RANGES and len(qrs) == bd.MAX_Q_RANGES
+
+    def rows(t, rs):
+        return [t[:, (L if s == CLEAN else 0) + p0:(L if s == CLEAN else 0) + p0 + n].contiguous() for s, p0, n in rs]
+
+    qs, dos, ks, vs = rows(q, qrs), rows(do, qrs), rows(k, krs), rows(v, krs)
+    p = bd.make_problem(1, L, M, Hq, Hkv, D, torch.bfloat16, out_f32=True)
+    QR, KR = [Range(*r) for r in qrs], [Range(*r) for r in krs]
+    qd, dod = [t.to(DEV) for t in qs], [t.to(DEV) for t in dos]
+    kd, vd = [t.to(DEV) for t in ks], [t.to(DEV) for t in vs]
+    od = [torch.empty(t.shape, dtype=torch.float32, device=DEV) for t in qd]
+    ld = [torch.empty((1, Hq, t.shape[1]), dtype=torch.float32, device=DEV) for t in qd]
+    bd.attn_fwd(p, QR, qd, od, ld, KR, kd, vd)
+    dqd = [torch.empty(t.shape, dtype=torch.float32, device=DEV) for t in qd]
+    dkd = [torch.empty(t.shape, dtype=torch.float32, device=DEV) for t in kd]
+    dvd = [torch.empty(t.shape, dtype=torch.float32, device=DEV) for t in vd]
+    ws = torch.empty(bd.attn_bwd_workspace_bytes(p, QR), dtype=torch.uint8, device=DEV)
+    bd.attn_bwd(p, QR, qd, od, ld, dod, dqd, KR, kd, vd, dkd, dvd, ws)
+    torch.cuda.synchronize()
+    qall, doall = torch.cat(qs, dim=1), torch.cat(dos, dim=1)
+    kall, vall = torch.cat(ks, dim=1), torch.cat(vs, dim=1)
+    O, LSE = oracle.fwd(qall, kall, vall, qrs, krs, M)
+    dQ, dK, dV = oracle.bwd(qall, kall, vall, O, LSE, doall, qrs, krs, M)
+    cat1 = lambda ts: torch.cat([t.cpu() for t in ts], dim=1)
+    assert_close("max ranges O", cat1(od), O, torch.bfloat16)
+    assert_close("max ranges LSE", torch.cat([t.cpu() for t in ld], dim=2), LSE, torch.bfloat16)
+    assert_close("max ranges dQ", cat1(dqd), dQ, torch.bfloat16)
+    assert_close("max ranges dK", cat1(dkd), dK, torch.bfloat16)
+    assert_close("max ranges dV", cat1(dvd), dV, torch.bfloat16)
