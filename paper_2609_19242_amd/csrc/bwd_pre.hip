@@ -5,7 +5,8 @@
 // L2[b][h][row] = LSE * log2(e) (+inf for rows that see no key, so that
 // exp2(s - L2) is 0 for them), the form the dK/dV kernel stages into LDS.
 // One thread per 8 consecutive head_dim elements; the D/8 threads of one
-// (row, head) are adjacent lanes and reduce with cross-lane shuffles.
+// (row, head) are adjacent lanes and reduce with cross-lane shuffles.  O and
+// dO are read once, with the non-temporal cache policy.
 #include "common.hpp"
 #include "device.hpp"
 
@@ -33,7 +34,7 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(const AttnArgs a) {
   if (ok) {
     float o[8], d[8];
     if constexpr (sizeof(TO) == 2) {
-      const bf16x8 x = *(const bf16x8*)((const bf16*)qr.o + off);
+      const bf16x8 x = __builtin_bit_cast(bf16x8, __builtin_nontemporal_load((const u32x4*)((const bf16*)qr.o + off)));
 #pragma unroll
       for (int e = 0; e < 8; ++e) o[e] = (float)x[e];
     } else {
@@ -41,7 +42,7 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(const AttnArgs a) {
       for (int e = 0; e < 8; ++e) o[e] = ((const float*)qr.o)[off + e];
     }
     if constexpr (sizeof(T) == 2) {
-      const bf16x8 x = *(const bf16x8*)((const bf16*)qr.dO + off);
+      const bf16x8 x = __builtin_bit_cast(bf16x8, __builtin_nontemporal_load((const u32x4*)((const bf16*)qr.dO + off)));
 #pragma unroll
       for (int e = 0; e < 8; ++e) d[e] = (float)x[e];
     } else {
