@@ -186,9 +186,22 @@ def attn_partial_fwd(p: Problem, qr: Range, q, o, lse, kr: Range, k, v, stream=N
 
 def lse_merge(o_parts, lse_parts, o, lse, stream=None):
     """``bdlm_lse_merge`` of partials shaped ``[batch][rows][heads][d]`` / ``[batch][heads][rows]``."""
+    if not isinstance(o, torch.Tensor) or o.dim() != 4:
+        raise ValueError("o must be a [batch][rows][heads][head_dim] tensor")
     B, R, H, D = o.shape
-    pdt = _dtype_code(o_parts[0].dtype)
-    _check(lib().bdlm_lse_merge(B, R, H, D, len(o_parts), _parr(o_parts), _parr(lse_parts), pdt,
+    if len(o_parts) != len(lse_parts) or not o_parts:
+        raise ValueError("need one LSE per partial output and at least one part")
+    _dtype_code(o.dtype)
+    pdt = o_parts[0].dtype
+    _dtype_code(pdt)
+    for j, (op, lp) in enumerate(zip(o_parts, lse_parts)):
+        _expect(f"o_parts[{j}]", op, pdt, o.shape)
+        _expect(f"lse_parts[{j}]", lp, torch.float32, (B, H, R))
+    _expect("o", o, o.dtype, o.shape)
+    _expect("lse", lse, torch.float32, (B, H, R))
+    _on_device(o.device, o=o, lse=lse, **{f"o_parts[{j}]": t for j, t in enumerate(o_parts)},
+               **{f"lse_parts[{j}]": t for j, t in enumerate(lse_parts)})
+    _check(lib().bdlm_lse_merge(B, R, H, D, len(o_parts), _parr(o_parts), _parr(lse_parts), _dtype_code(pdt),
                                 _ptr(o), _ptr(lse), _dtype_code(o.dtype), _stream(stream)))
 
 
@@ -234,13 +247,44 @@ def _joint_ptrs(t: torch.Tensor, L: int):
     return [t.data_ptr(), t.data_ptr() + step]
 
 
+def _expect(name, t, dtype, shape):
+    """Reject a tensor of the wrong type, dtype, shape or layout before any pointer reaches the library."""
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor, got {type(t).__name__}")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _on_device(device, **tensors):
+    for name, t in tensors.items():
+        if not t.is_cuda or t.device != device:
+            raise ValueError(f"{name} must be on {device}, got {t.device}")
+
+
 def _check_joint(q, k, v):
-    for name, t in (("q", q), ("k", k), ("v", v)):
-        if not t.is_cuda or not t.is_contiguous():
-            raise ValueError(f"{name} must be a contiguous device tensor")
-    if q.dim() != 4 or k.shape != v.shape or q.shape[0] != k.shape[0] or q.shape[1] != k.shape[1] \
-            or q.shape[3] != k.shape[3] or q.shape[1] % 2:
-        raise ValueError(f"bad joint shapes q{tuple(q.shape)} k{tuple(k.shape)} v{tuple(v.shape)}")
+    """Packed ``[x_t ; x]`` inputs: q ``[B][2L][Hq][D]``, k and v ``[B][2L][Hkv][D]``, one dtype."""
+    if not isinstance(q, torch.Tensor) or q.dim() != 4 or q.shape[1] % 2:
+        raise ValueError(f"q must be a [batch][2L][heads][head_dim] tensor, got "
+                         f"{tuple(q.shape) if isinstance(q, torch.Tensor) else type(q).__name__}")
+    _dtype_code(q.dtype)
+    B, n, _, D = q.shape
+    if not isinstance(k, torch.Tensor) or k.dim() != 4:
+        raise ValueError("k must be a [batch][2L][kv_heads][head_dim] tensor")
+    _expect("q", q, q.dtype, q.shape)
+    _expect("k", k, q.dtype, (B, n, k.shape[2], D))
+    _expect("v", v, q.dtype, k.shape)
+
+
+def _check_ws(workspace, device):
+    if workspace is None:
+        return
+    if not isinstance(workspace, torch.Tensor) or not workspace.is_contiguous():
+        raise ValueError("workspace must be a contiguous tensor")
+    _on_device(device, workspace=workspace)
 
 
 def joint_fwd(q, k, v, block_size: int, clean_intra: int = CLEAN_INTRA_CAUSAL, scale: float = 0.0,
@@ -256,8 +300,18 @@ def joint_fwd(q, k, v, block_size: int, clean_intra: int = CLEAN_INTRA_CAUSAL, s
     p = make_problem(B, L, block_size, Hq, k.shape[2], D, q.dtype, scale, clean_intra, out_f32, hilo,
                      window, clean_prefix)
     odt = torch.float32 if out_f32 else q.dtype
-    o, lse = out if out is not None else (torch.empty(q.shape, dtype=odt, device=q.device),
-                                          torch.empty((B, Hq, n), dtype=torch.float32, device=q.device))
+    if out is not None:
+        if len(out) != 2:
+            raise ValueError("out must be (o, lse)")
+        o, lse = out
+        _expect("o", o, odt, q.shape)
+        _expect("lse", lse, torch.float32, (B, Hq, n))
+    _on_device(q.device, q=q, k=k, v=v)
+    if out is None:
+        o = torch.empty(q.shape, dtype=odt, device=q.device)
+        lse = torch.empty((B, Hq, n), dtype=torch.float32, device=q.device)
+    else:
+        _on_device(q.device, o=o, lse=lse)
     r = joint_ranges(L)
     lp = [lse.data_ptr(), lse.data_ptr() + L * 4]
     attn_fwd(p, r, _joint_ptrs(q, L), _joint_ptrs(o, L), lp, r, _joint_ptrs(k, L), _joint_ptrs(v, L), stream)
@@ -275,10 +329,20 @@ def joint_bwd(q, k, v, o, lse, do, block_size: int, clean_intra: int = CLEAN_INT
                      window, clean_prefix)
     r = joint_ranges(L)
     odt = torch.float32 if out_f32 else q.dtype
-    if o.dtype != odt:
-        raise TypeError(f"o must be {odt}")
+    _expect("o", o, odt, q.shape)
+    _expect("lse", lse, torch.float32, (B, Hq, n))
+    _expect("do", do, q.dtype, q.shape)
+    if out is not None:
+        if len(out) != 3:
+            raise ValueError("out must be (dq, dk, dv)")
+        for name, t, like in zip(("dq", "dk", "dv"), out, (q, k, v)):
+            _expect(name, t, odt, like.shape)
+    _on_device(q.device, q=q, k=k, v=v, o=o, lse=lse, do=do)
+    _check_ws(workspace, q.device)
     if out is None:
         out = tuple(torch.empty(t.shape, dtype=odt, device=q.device) for t in (q, k, v))
+    else:
+        _on_device(q.device, dq=out[0], dk=out[1], dv=out[2])
     dq, dk, dv = out
     if workspace is None:
         workspace = torch.empty(attn_bwd_workspace_bytes(p, r), dtype=torch.uint8, device=q.device)

@@ -412,3 +412,61 @@ def test_per_range_backward_with_merged_stats_equals_unsplit():
         np.testing.assert_allclose(dk, dK[:, off:off + n], rtol=0, atol=1e-13)
         np.testing.assert_allclose(dv, dV[:, off:off + n], rtol=0, atol=1e-13)
     np.testing.assert_allclose(dQs, dQ, rtol=0, atol=1e-13)
+
+
+# ------------------------------------------------ head and row subsets of the oracle
+# The full-size GPU tests call the oracle on a subset of query heads and rows.
+# Pinned here against the full call by two facts that do not re-type the
+# oracle: heads and query rows are independent in the forward, and in the
+# backward a query row whose upstream gradient dO is zero contributes nothing
+# to dK or dV (its dP and D vanish, so dS = 0 and P^T dO = 0).
+@pytest.mark.parametrize("reading", READINGS)
+def test_subset_heads_and_rows_equal_slices_of_the_full_call(reading):
+    L, M, Hq, Hkv, d = 24, 4, 4, 2, 8
+    q, k, v, do = joint_inputs(L, Hq, Hkv, d, seed=71, batch=2)
+    r = oracle.joint_ranges(L)
+    s_all, p_all = oracle.rows_of(r)
+    O, LSE = oracle.fwd(q, k, v, r, r, M, clean_intra=reading)
+    dQ, dK, dV = oracle.bwd(q, k, v, O, LSE, do, r, r, M, clean_intra=reading)
+
+    # forward: q_rows and heads select rows and heads of the full result
+    rows = np.array([0, 3, 5, L - 1, L, L + 7, 2 * L - 1])
+    hs = [1, 2]
+    Os, Ls = oracle.fwd(q, k, v, r, r, M, clean_intra=reading, heads=hs, q_rows=rows)
+    np.testing.assert_allclose(Os, O[:, rows][:, :, hs], rtol=0, atol=1e-13)
+    np.testing.assert_allclose(Ls, LSE[:, hs][:, :, rows], rtol=0, atol=1e-13)
+    # the same rows passed as single-row ranges (the form the full-size GPU tests use)
+    single = [(int(s_all[i]), int(p_all[i]), 1) for i in rows]
+    Os2, Ls2 = oracle.fwd(q[:, rows], k, v, single, r, M, clean_intra=reading, heads=hs)
+    np.testing.assert_allclose(Os2, Os, rtol=0, atol=1e-13)
+    np.testing.assert_allclose(Ls2, Ls, rtol=0, atol=1e-13)
+
+    # backward over one complete GQA group (KV head 1 = query heads 2, 3): its dQ
+    # rows and the group's whole dK/dV
+    grp = [2, 3]
+    dQg, dKg, dVg = oracle.bwd(q, k, v, O[:, :, grp], LSE[:, grp], do[:, :, grp], r, r, M, clean_intra=reading,
+                               heads=grp)
+    np.testing.assert_allclose(dQg, dQ[:, :, grp], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(dKg[:, :, 1], dK[:, :, 1], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(dVg[:, :, 1], dV[:, :, 1], rtol=0, atol=1e-12)
+    assert not dKg[:, :, 0].any() and not dVg[:, :, 0].any()
+
+    # one head of a group: dK/dV equal the full call with dO zero on every other head
+    do1 = np.zeros_like(do)
+    do1[:, :, 2] = do[:, :, 2]
+    _, dK1, dV1 = oracle.bwd(q, k, v, O, LSE, do1, r, r, M, clean_intra=reading)
+    _, dKh, dVh = oracle.bwd(q, k, v, O[:, :, [2]], LSE[:, [2]], do[:, :, [2]], r, r, M, clean_intra=reading,
+                             heads=[2])
+    np.testing.assert_allclose(dKh, dK1, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(dVh, dV1, rtol=0, atol=1e-12)
+
+    # a subset of query rows as single-row ranges: their dQ rows, and dK/dV equal
+    # the full call with dO zero on every other row
+    dQs, dKs, dVs = oracle.bwd(q[:, rows], k, v, O[:, rows], LSE[:, :, rows], do[:, rows], single, r, M,
+                               clean_intra=reading)
+    np.testing.assert_allclose(dQs, dQ[:, rows], rtol=0, atol=1e-12)
+    dor = np.zeros_like(do)
+    dor[:, rows] = do[:, rows]
+    _, dKr, dVr = oracle.bwd(q, k, v, O, LSE, dor, r, r, M, clean_intra=reading)
+    np.testing.assert_allclose(dKs, dKr, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(dVs, dVr, rtol=0, atol=1e-12)
