@@ -82,13 +82,13 @@ def per_kernel(records):
     return {k: {"avg_ms": v[0] / v[1], "launches": v[1]} for k, v in out.items()}
 
 
-def bench_32k(torch, bd, synth, steps, warmup):
+def bench_32k(torch, bd, synth, steps, warmup, reading=0):
     w = synth.WORKLOADS["32k"]
     dev = "cuda"
     q, k, v, do = synth.make_joint(w, device=dev)
     B, n, Hq, D = q.shape
     L, M = w.L, w.block_size
-    p = bd.make_problem(B, L, M, Hq, w.kv_heads, D, torch.bfloat16)
+    p = bd.make_problem(B, L, M, Hq, w.kv_heads, D, torch.bfloat16, clean_intra=reading)
     r = bd.joint_ranges(L)
     pairs = bd.visible_pairs(p, r, r)
     fl = bd.useful_flops(pairs, Hq, B, D)
@@ -98,8 +98,8 @@ def bench_32k(torch, bd, synth, steps, warmup):
     ws = torch.empty(bd.attn_bwd_workspace_bytes(p, r), dtype=torch.uint8, device=dev)
 
     def step():
-        bd.joint_fwd(q, k, v, M, out=(o, lse))
-        bd.joint_bwd(q, k, v, o, lse, do, M, out=(dq, dk, dv), workspace=ws)
+        bd.joint_fwd(q, k, v, M, out=(o, lse), clean_intra=reading)
+        bd.joint_bwd(q, k, v, o, lse, do, M, out=(dq, dk, dv), workspace=ws, clean_intra=reading)
 
     for _ in range(warmup):
         step()
@@ -137,7 +137,8 @@ def bench_32k(torch, bd, synth, steps, warmup):
     bwd_ms = sum(kern[k]["avg_ms"] for k in ("bwd_pre", "bwd_dkdv_bf16", "bwd_dq_bf16") if k in kern)
     res = {"ms_per_step": ms, "median_ms_per_step": median_ms, "fwd_ms": fwd_ms, "bwd_ms": bwd_ms,
            "wall_s": wall, "pairs_per_head": pairs, "flops": fl, "kernels": kern,
-           "roofline": roof, "value": fl["total"] / (ms * 1e-3) / 1e12, "workload": w}
+           "roofline": roof, "value": fl["total"] / (median_ms * 1e-3) / 1e12,
+           "mean_value": fl["total"] / (ms * 1e-3) / 1e12, "workload": w}
     del q, k, v, do, o, lse, dq, dk, dv, ws
     torch.cuda.empty_cache()
     return res
@@ -304,33 +305,37 @@ def bench_ext(torch, bd, synth, steps, warmup):
 
 
 def bench_configs(torch, bd, synth, steps, warmup):
-    """Step time of the other joint workloads (parity-test configurations, not
-    bench lines): 4k (batch 2, block 32) and 128k (block 128, 64/8 heads, 1% of
-    keys x8) with and without the two-term P/dS products it needs for parity."""
+    """Step time of the other joint workloads: 4k (batch 2, block 32; bf16 outputs,
+    single-term products, as the headline) and 128k (block 128, 64/8 heads, 1% of
+    keys x8) in the arithmetic its parity needs: fp32 outputs and two-term P V
+    and dS K products."""
     out = {}
-    for name, hilo in (("4k", False), ("128k", False), ("128k", True)):
+    legs = (("4k", dict(), steps, warmup),
+            ("128k", dict(out_f32=True, hilo=bd.HILO_PV | bd.HILO_DQ), max(2, steps // 4), 1))
+    for name, arith, n_steps, n_warm in legs:
         w = synth.WORKLOADS[name]
         q, k, v, do = synth.make_joint(w, device="cuda")
         B, n, Hq, D = q.shape
         L, M = w.L, w.block_size
-        p = bd.make_problem(B, L, M, Hq, w.kv_heads, D, torch.bfloat16, hilo=hilo)
+        p = bd.make_problem(B, L, M, Hq, w.kv_heads, D, torch.bfloat16, **arith)
         r = bd.joint_ranges(L)
         pairs = bd.visible_pairs(p, r, r)
-        o, lse = torch.empty_like(q), torch.empty((B, Hq, n), dtype=torch.float32, device="cuda")
-        dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+        odt = torch.float32 if arith.get("out_f32") else torch.bfloat16
+        o, lse = torch.empty(q.shape, dtype=odt, device="cuda"), torch.empty((B, Hq, n), dtype=torch.float32,
+                                                                              device="cuda")
+        dq, dk, dv = (torch.empty(t.shape, dtype=odt, device="cuda") for t in (q, k, v))
         ws = torch.empty(bd.attn_bwd_workspace_bytes(p, r), dtype=torch.uint8, device="cuda")
 
         def step():
-            bd.joint_fwd(q, k, v, M, out=(o, lse), hilo=hilo)
-            bd.joint_bwd(q, k, v, o, lse, do, M, out=(dq, dk, dv), workspace=ws, hilo=hilo)
+            bd.joint_fwd(q, k, v, M, out=(o, lse), **arith)
+            bd.joint_bwd(q, k, v, o, lse, do, M, out=(dq, dk, dv), workspace=ws, **arith)
 
-        ms, kern = _timed_steps(torch, bd, step, steps, warmup)
+        ms, kern = _timed_steps(torch, bd, step, n_steps, n_warm)
         fl = bd.useful_flops(pairs, Hq, B, D)
-        out[name + ("-hilo" if hilo else "")] = {
-            "workload": w.describe() + (", hilo" if hilo else ""), "ms_per_step": ms,
-            "useful_tflops": fl["total"] / (ms * 1e-3) / 1e12, "pairs_per_head": pairs, "kernels": kern}
-        print(f"[bench] {name}{' hilo' if hilo else ''}: {ms:.3f} ms/step, "
-              f"{out[name + ('-hilo' if hilo else '')]['useful_tflops']:.1f} useful TFLOP/s", flush=True)
+        desc = w.describe() + (", fp32 outputs, two-term P V and dS K" if arith else ", bf16 outputs")
+        out[name] = {"workload": desc, "ms_per_step": ms, "steps": n_steps,
+                     "useful_tflops": fl["total"] / (ms * 1e-3) / 1e12, "pairs_per_head": pairs, "kernels": kern}
+        print(f"[bench] {name}: {ms:.3f} ms/step, {out[name]['useful_tflops']:.1f} useful TFLOP/s", flush=True)
         del q, k, v, do, o, lse, dq, dk, dv, ws
         torch.cuda.empty_cache()
     return out
@@ -354,6 +359,10 @@ def cpu_baseline(bd, synth, budget_s):
     order = np.random.default_rng(0).permutation(n_chunks)
     pairs = 0
     rows_done = 0
+    cores = len(os.sched_getaffinity(0))
+    from threadpoolctl import threadpool_limits, threadpool_info
+    limiter = threadpool_limits(limits=cores, user_api="blas")
+    blas_threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
     t0 = time.perf_counter()
     for c in order:
         rows = list(range(c * chunk_rows, (c + 1) * chunk_rows))
@@ -366,13 +375,10 @@ def cpu_baseline(bd, synth, budget_s):
         if time.perf_counter() - t0 >= budget_s:
             break
     el = time.perf_counter() - t0
-    try:
-        from threadpoolctl import threadpool_info
-        cores = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
-    except Exception:
-        cores = len(os.sched_getaffinity(0))
+    limiter.restore_original_limits()
     flops = 14 * D * pairs
-    return {"value": flops / el / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+    return {"value": flops / el / 1e12, "unit": "TFLOP/s", "cores": blas_threads, "cores_available": cores,
+            "kind": "oracle",
             "sample": f"{rows_done} query rows (random 64-row chunks) x 1 head of the 32K workload, "
                       f"fp64 forward+backward over all their visible keys ({pairs} pairs) in {el:.1f} s",
             "seconds": el}
@@ -387,6 +393,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-csbp", action="store_true")
     ap.add_argument("--no-ext", action="store_true", help="skip the sliding-window and drafter legs")
+    ap.add_argument("--no-configs", action="store_true", help="skip the 4k and 128k workload legs")
     ap.add_argument("--configs-only", action="store_true",
                     help="time only the 4k and 128k joint workloads and print their result")
     ap.add_argument("--ext-only", action="store_true",
@@ -431,7 +438,15 @@ def main():
         print(json.dumps({"csbp256k": res}), flush=True)
         return
     main_res = bench_32k(torch, bd, synth, args.steps, args.warmup)
-    print(f"[bench] 32k: {main_res['ms_per_step']:.3f} ms/step, {main_res['value']:.1f} useful TFLOP/s", flush=True)
+    print(f"[bench] 32k: {main_res['median_ms_per_step']:.3f} ms/step (median), {main_res['value']:.1f} useful TFLOP/s",
+          flush=True)
+    blk = bench_32k(torch, bd, synth, max(3, args.steps // 2), 1, reading=1)
+    block_reading = {"workload": blk["workload"].describe() + ", clean-to-clean block reading",
+                     "median_ms_per_step": blk["median_ms_per_step"], "useful_tflops": blk["value"],
+                     "pairs_per_head": blk["pairs_per_head"], "fwd_ms": blk["fwd_ms"], "bwd_ms": blk["bwd_ms"]}
+    print(f"[bench] 32k block reading: {blk['median_ms_per_step']:.3f} ms/step, {blk['value']:.1f} useful TFLOP/s",
+          flush=True)
+    configs = None if args.no_configs else bench_configs(torch, bd, synth, args.steps, args.warmup)
     csbp = None if args.no_csbp else bench_csbp(torch, bd, synth, max(2, args.steps // 2), 1)
     if csbp:
         print(f"[bench] csbp256k: {csbp['ms_per_step']:.3f} ms/step; with clean-shard queries "
@@ -449,7 +464,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": main_res["ms_per_step"],
+        "ms_per_step": main_res["median_ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -459,7 +474,8 @@ def main():
                    "heads": w.heads, "kv_heads": w.kv_heads, "head_dim": w.head_dim, "clean_intra": "causal",
                    "parallelism": "single GPU"},
         "mfma_util_useful": main_res["value"] / PEAK_BF16_TFLOPS,
-        "median_ms_per_step": main_res["median_ms_per_step"],
+        "mean_ms_per_step": main_res["ms_per_step"],
+        "value_from_mean_step": main_res["mean_value"],
         "fwd_ms": main_res["fwd_ms"],
         "bwd_ms": main_res["bwd_ms"],
         "fwd_useful_tflops": main_res["flops"]["fwd"] / (main_res["fwd_ms"] * 1e-3) / 1e12,
@@ -470,8 +486,10 @@ def main():
         "roofline": main_res["roofline"],
         "kernels": main_res["kernels"],
         "cpu_baseline": cpu,
+        "block_reading_32k": block_reading,
         "csbp256k": csbp,
         "mask_ext": ext,
+        "configs": configs,
     }
     print(json.dumps(line), flush=True)
 

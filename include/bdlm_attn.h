@@ -90,6 +90,12 @@ typedef enum {
   BDLM_CLEAN_INTRA_BLOCK = 1   /* clean query sees every clean key of its own and earlier blocks */
 } bdlm_clean_intra;
 
+/* Bits of bdlm_problem.hilo: which products carry P or dS as two bf16 terms. */
+#define BDLM_HILO_PV 1   /* forward O += P V */
+#define BDLM_HILO_DKDV 2 /* backward dV += P^T dO and dK += dS^T Q */
+#define BDLM_HILO_DQ 4   /* backward dQ += dS K */
+#define BDLM_HILO_ALL 7
+
 /* Limits of one call (kernel-argument capacity). */
 #define BDLM_MAX_Q_RANGES 4
 #define BDLM_MAX_K_RANGES 32
@@ -107,11 +113,12 @@ typedef struct {
   float scale;        /* softmax scale; <= 0 selects 1 / sqrt(head_dim) */
   int32_t clean_intra;/* bdlm_clean_intra */
   int32_t out_f32;    /* 0: O, dQ, dK, dV in `dtype`; 1: in fp32 (the fp32 accumulators, unrounded) */
-  int32_t hilo;       /* bf16 path: 0 rounds the softmax probabilities P and dS = P (dP - D) to
-                         bf16 for the P V, P^T dO, dS K and dS^T Q products; 1 carries each as a
-                         two-term bf16 sum hi + lo (about 16 significant bits, up to 1.5x the
-                         matrix work of those products), for inputs with large scores or |dS|,
-                         e.g. keys of large norm.  Ignored by the fp32 path. */
+  int32_t hilo;       /* bf16 path: a mask of BDLM_HILO_* bits.  A product whose bit is clear takes
+                         its operand P (softmax probabilities) or dS = P (dP - D) rounded to bf16;
+                         a product whose bit is set takes it as a two-term bf16 sum hi + lo (about
+                         16 significant bits, twice the matrix work of that product).  For inputs
+                         with large scores or |dS|, e.g. keys of large norm.  Ignored by the fp32
+                         path. */
   int64_t window;     /* 0: no limit.  > 0: a query sees only the last `window` positions of its clean
                          context (sliding-window layers; see "Mask generalisations" above) */
   const int32_t* clean_prefix; /* NULL, or a device array of L / block_size ints: the end of the clean

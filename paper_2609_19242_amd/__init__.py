@@ -22,6 +22,7 @@ import torch  # noqa: F401  (load torch's HIP runtime first)
 __all__ = [
     "Problem", "Range", "BdlmError", "lib", "library_path",
     "BF16", "F32", "CLEAN", "CORRUPTED", "CLEAN_INTRA_CAUSAL", "CLEAN_INTRA_BLOCK",
+    "HILO_PV", "HILO_DKDV", "HILO_DQ", "HILO_ALL",
     "make_problem", "joint_ranges", "attn_fwd", "attn_partial_fwd", "lse_merge",
     "attn_bwd_workspace_bytes", "attn_bwd", "visible_pairs",
     "joint_fwd", "joint_bwd", "timing_enable", "timing_collect", "useful_flops",
@@ -30,6 +31,9 @@ __all__ = [
 BF16, F32 = 0, 1
 CLEAN, CORRUPTED = 0, 1
 CLEAN_INTRA_CAUSAL, CLEAN_INTRA_BLOCK = 0, 1
+# bdlm_problem.hilo bits: products that take P or dS as two bf16 terms
+HILO_PV, HILO_DKDV, HILO_DQ = 1, 2, 4
+HILO_ALL = HILO_PV | HILO_DKDV | HILO_DQ
 MAX_Q_RANGES, MAX_K_RANGES, MAX_MERGE_PARTS = 4, 32, 32
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -151,8 +155,9 @@ def _dtype_code(dt: torch.dtype) -> int:
 
 def make_problem(batch: int, L: int, block_size: int, heads: int, kv_heads: int, head_dim: int,
                  dtype, scale: float = 0.0, clean_intra: int = CLEAN_INTRA_CAUSAL, out_f32: bool = False,
-                 hilo: bool = False, window: int = 0, clean_prefix: Optional[torch.Tensor] = None) -> Problem:
-    """Problem record.  ``window`` limits every query to the last ``window`` positions of its clean
+                 hilo=False, window: int = 0, clean_prefix: Optional[torch.Tensor] = None) -> Problem:
+    """Problem record.  ``hilo`` is a mask of ``HILO_*`` bits (``True`` means all of them): the
+    products that take P or dS as two bf16 terms.  ``window`` limits every query to the last ``window`` positions of its clean
     context (0: no limit); ``clean_prefix`` is an int32 device tensor of ``L // block_size`` entries,
     the end of corrupted block b's clean context (DFlash2 anchors), kept alive by the caller until the
     kernels that use it have run."""
@@ -163,8 +168,9 @@ def make_problem(batch: int, L: int, block_size: int, heads: int, kv_heads: int,
                 or clean_prefix.numel() != L // block_size:
             raise ValueError("clean_prefix must be a contiguous int32 device tensor of L // block_size entries")
         pref = clean_prefix.data_ptr()
+    hmask = HILO_ALL if hilo is True else int(hilo)
     return Problem(batch, L, block_size, heads, kv_heads, head_dim, code, scale, clean_intra, int(bool(out_f32)),
-                   int(bool(hilo)), int(window), pref)
+                   hmask, int(window), pref)
 
 
 def joint_ranges(L: int) -> List[Range]:
@@ -288,7 +294,7 @@ def _check_ws(workspace, device):
 
 
 def joint_fwd(q, k, v, block_size: int, clean_intra: int = CLEAN_INTRA_CAUSAL, scale: float = 0.0,
-              out_f32: bool = False, out: Optional[tuple] = None, stream=None, hilo: bool = False,
+              out_f32: bool = False, out: Optional[tuple] = None, stream=None, hilo=False,
               window: int = 0, clean_prefix: Optional[torch.Tensor] = None):
     """Fused forward over packed ``[x_t ; x]`` tensors ``q [B][2L][Hq][D]``, ``k, v [B][2L][Hkv][D]``.
 
@@ -320,7 +326,7 @@ def joint_fwd(q, k, v, block_size: int, clean_intra: int = CLEAN_INTRA_CAUSAL, s
 
 def joint_bwd(q, k, v, o, lse, do, block_size: int, clean_intra: int = CLEAN_INTRA_CAUSAL, scale: float = 0.0,
               out_f32: bool = False, out: Optional[tuple] = None, workspace: Optional[torch.Tensor] = None,
-              stream=None, hilo: bool = False, window: int = 0, clean_prefix: Optional[torch.Tensor] = None):
+              stream=None, hilo=False, window: int = 0, clean_prefix: Optional[torch.Tensor] = None):
     """Backward of :func:`joint_fwd`; returns ``(dq, dk, dv)`` (fp32 when ``out_f32``; ``o`` must match)."""
     _check_joint(q, k, v)
     B, n, Hq, D = q.shape

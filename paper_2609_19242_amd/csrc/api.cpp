@@ -92,7 +92,8 @@ bdlm_status check_problem(const bdlm_problem* p) {
     return fail(BDLM_ERR_INVALID, "clean_intra %d is not a bdlm_clean_intra value", p->clean_intra);
   if (!std::isfinite(p->scale)) return fail(BDLM_ERR_INVALID, "scale is not finite");
   if (p->out_f32 != 0 && p->out_f32 != 1) return fail(BDLM_ERR_INVALID, "out_f32 must be 0 or 1");
-  if (p->hilo != 0 && p->hilo != 1) return fail(BDLM_ERR_INVALID, "hilo must be 0 or 1");
+  if (p->hilo < 0 || p->hilo > BDLM_HILO_ALL)
+    return fail(BDLM_ERR_INVALID, "hilo must be a mask of BDLM_HILO_* bits (0..%d, got %d)", BDLM_HILO_ALL, p->hilo);
   if (p->window < 0 || p->window >= kMaxPos)
     return fail(BDLM_ERR_INVALID, "window must be in [0, 2^30) (got %lld)", (long long)p->window);
   if (p->clean_prefix && (reinterpret_cast<uintptr_t>(p->clean_prefix) & 3u) != 0)

@@ -432,10 +432,10 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, int head_dim, hipStream_t s) {
   const int n = a.total_tiles * a.kv_heads * a.batch;
   if (n == 0) return hipSuccess;
   if (head_dim == 128) {
-    if (a.hilo) launch_nq<128, true>(a, n, s);
+    if (a.hilo & kHiloDkDv) launch_nq<128, true>(a, n, s);
     else launch_nq<128, false>(a, n, s);
   } else {
-    if (a.hilo) launch_nq<64, true>(a, n, s);
+    if (a.hilo & kHiloDkDv) launch_nq<64, true>(a, n, s);
     else launch_nq<64, false>(a, n, s);
   }
   return hipGetLastError();

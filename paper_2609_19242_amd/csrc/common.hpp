@@ -21,6 +21,11 @@ enum : int { kClean = 0, kCorrupted = 1 };
 enum : int { kIntraCausal = 0, kIntraBlock = 1 };
 
 constexpr int kMaxQ = 4;
+// Products that take their P or dS operand as two bf16 terms (the hilo mask of
+// the problem; the values of the BDLM_HILO_* bits of the C ABI).
+constexpr int kHiloPv = 1;    // forward P V
+constexpr int kHiloDkDv = 2;  // backward P^T dO and dS^T Q (dK/dV kernel)
+constexpr int kHiloDq = 4;    // backward dS K (dQ kernel)
 constexpr int kMaxK = 32;
 constexpr int kMaxParts = 32;
 constexpr int kBig = 0x3fffffff;  // "to the end of the stream" (positions stay below 2^30)
@@ -152,7 +157,7 @@ struct AttnArgs {
   int32_t total_tiles;   // flattened tiles (query tiles for fwd, key tiles for bwd)
   int32_t interleave;    // fwd: query ranges have equal tile counts, visit them round-robin
   int32_t out_f32;       // O, dQ, dK, dV are fp32 (else the input dtype)
-  int32_t hilo;          // P and dS enter their products as bf16 hi + lo
+  int32_t hilo;          // kHilo* bits: products whose P or dS operand is bf16 hi + lo
   int32_t order[kMaxK];  // bwd: visiting order of key ranges (heaviest first)
   QRangeArg qr[kMaxQ];
   KRangeArg kr[kMaxK];

@@ -301,10 +301,10 @@ hipError_t launch_fwd_bf16(const AttnArgs& a, int head_dim, hipStream_t s) {
   const int n = a.total_tiles * a.heads * a.batch;
   if (n == 0) return hipSuccess;
   if (head_dim == 128) {
-    if (a.hilo) hipLaunchKernelGGL((fwd_bf16_kernel<128, NW, true>), dim3(n), dim3(NW * 64), 0, s, a);
+    if (a.hilo & kHiloPv) hipLaunchKernelGGL((fwd_bf16_kernel<128, NW, true>), dim3(n), dim3(NW * 64), 0, s, a);
     else hipLaunchKernelGGL((fwd_bf16_kernel<128, NW, false>), dim3(n), dim3(NW * 64), 0, s, a);
   } else {
-    if (a.hilo) hipLaunchKernelGGL((fwd_bf16_kernel<64, NW, true>), dim3(n), dim3(NW * 64), 0, s, a);
+    if (a.hilo & kHiloPv) hipLaunchKernelGGL((fwd_bf16_kernel<64, NW, true>), dim3(n), dim3(NW * 64), 0, s, a);
     else hipLaunchKernelGGL((fwd_bf16_kernel<64, NW, false>), dim3(n), dim3(NW * 64), 0, s, a);
   }
   return hipGetLastError();

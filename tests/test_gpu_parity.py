@@ -28,26 +28,32 @@ def run_joint(q, k, v, do, M, reading, out_f32, hilo=False):
     return o, lse, dq, dk, dv
 
 
-def check_joint(q, k, v, do, M, reading, dtype, heads=None, tag="", out_f32=True, hilo=False):
+def check_joint(q, k, v, do, M, reading, dtype, heads=None, tag="", out_f32=True, hilo=False, outs=None):
     """GPU joint fwd+bwd against the oracle on the query heads ``heads`` (all by default).
 
-    Strict tolerance on fp32 outputs; with bf16 outputs (``out_f32=False``) the
-    bound adds the output rounding.
+    ``outs`` lists the output modes to run against one oracle result ("f32":
+    the fp32 accumulators, strict tolerance; "bf16": outputs rounded to bf16,
+    whose bound adds the output rounding, and whose backward reads the rounded
+    O); by default the single mode ``out_f32`` selects.  Returns the GPU
+    results of the last mode.
     """
     L = q.shape[1] // 2
-    o, lse, dq, dk, dv = run_joint(q, k, v, do, M, reading, out_f32, hilo)
+    outs = outs or (("f32",) if out_f32 else ("bf16",))
     hs = list(range(q.shape[2])) if heads is None else heads
     O, LSE = oracle.joint_fwd(q, k, v, L, M, clean_intra=reading, heads=hs)
     dQ, dK, dV = oracle.joint_bwd(q, k, v, O, LSE, do[:, :, hs], L, M, clean_intra=reading, heads=hs)
     kvs = sorted(set(h // (q.shape[2] // k.shape[2]) for h in hs))
-    assert_close(f"{tag} LSE", lse[:, hs], LSE, dtype)
-    pairs = (("O", o[:, :, hs], O), ("dQ", dq[:, :, hs], dQ), ("dK", dk[:, :, kvs], dK[:, :, kvs]),
-             ("dV", dv[:, :, kvs], dV[:, :, kvs]))
-    for name, got, ref in pairs:
-        if out_f32 or dtype == torch.float32:
-            assert_close(f"{tag} {name}", got, ref, dtype)
-        else:
-            assert_close_bf16_out(f"{tag} {name}", got, ref)
+    for mode in outs:
+        f32 = mode == "f32" or dtype == torch.float32
+        o, lse, dq, dk, dv = run_joint(q, k, v, do, M, reading, f32, hilo)
+        assert_close(f"{tag} [{mode} out] LSE", lse[:, hs], LSE, dtype)
+        pairs = (("O", o[:, :, hs], O), ("dQ", dq[:, :, hs], dQ), ("dK", dk[:, :, kvs], dK[:, :, kvs]),
+                 ("dV", dv[:, :, kvs], dV[:, :, kvs]))
+        for name, got, ref in pairs:
+            if f32:
+                assert_close(f"{tag} [{mode} out] {name}", got, ref, dtype)
+            else:
+                assert_close_bf16_out(f"{tag} [{mode} out] {name}", got, ref)
     return o, lse, dq, dk, dv
 
 
@@ -80,12 +86,32 @@ def test_workload_tiny_fp32(reading):
     check_joint(q, k, v, do, w.block_size, reading, torch.float32, tag=f"tiny r{reading}")
 
 
-def test_workload_4k_bf16_head_subset():
+@pytest.mark.parametrize("reading", [0, 1], ids=["causal", "block"])
+def test_workload_4k_bf16_head_subset(reading):
+    """The 4k workload (batch 2, L = 4096 + 4096, block 32, 32/8 heads): every row and
+    every key of KV groups {0, 7}, with fp32 and with bf16 outputs (bench.py's arithmetic)."""
     w = WORKLOADS["4k"]
     q, k, v, do = make_joint(w)
     hs = kv_group_heads(w.heads, w.kv_heads, [0, w.kv_heads - 1])
-    o, lse, *_ = check_joint(q, k, v, do, w.block_size, 0, torch.bfloat16, heads=hs, tag="4k")
+    o, lse, *_ = check_joint(q, k, v, do, w.block_size, reading, torch.bfloat16, heads=hs, tag=f"4k r{reading}",
+                             outs=("f32", "bf16"))
     assert torch.isfinite(o).all() and torch.isfinite(lse).all()
+
+
+@pytest.mark.parametrize("reading", [0, 1], ids=["causal", "block"])
+def test_complete_kv_group_8k_block64(reading):
+    """Element by element over one whole KV group at a size where clean keys are
+    seen by thousands of query rows: batch 1, L = 8192 + 8192, block 64, 32/8
+    heads, d 128; every row of query heads 0-3 (O, LSE, dQ) and every key of KV
+    head 0 (dK, dV summed over the group), with fp32 and with bf16 outputs."""
+    import synth
+    L, M, Hq, Hkv, D = 8192, 64, 32, 8, 128
+    q = synth.normal((1, 2 * L, Hq, D), 9000, torch.bfloat16)
+    k = synth.normal((1, 2 * L, Hkv, D), 9001, torch.bfloat16)
+    v = synth.normal((1, 2 * L, Hkv, D), 9002, torch.bfloat16)
+    do = synth.normal((1, 2 * L, Hq, D), 9003, torch.bfloat16)
+    check_joint(q, k, v, do, M, reading, torch.bfloat16, heads=[0, 1, 2, 3], tag=f"8k group0 r{reading}",
+                outs=("f32", "bf16"))
 
 
 # ------------------------------------------------------ partial + merge, CSBP
