@@ -209,16 +209,17 @@ def test_workload_drafter32k():
 
 def test_workload_128k():
     """128K with 1% of the keys scaled x8 (logits up to about +-40), in the arithmetic
-    that meets the bar there: fp32 outputs and two-term P in the forward P V and
-    two-term dS in the dQ kernel's dS K.  Single bf16 terms leave about 7e-2 in dQ,
-    through dS K (|dS| up to about 30) and through D = rowsum(dO O), which
-    inherits O's P rounding; with bf16 outputs D also inherits O's output
-    rounding (about 0.1 in dQ).  The dK/dV products stay single-term."""
-    joint_check(WORKLOADS["128k"], 0, n_random=8, hilo=bd.HILO_PV | bd.HILO_DQ)
+    that meets the bar there: fp32 outputs and every P and dS product in two bf16
+    terms.  Single terms fail in each kernel: P V and dS K leave about 7e-2 in dQ
+    (|dS| up to about 30, and D = rowsum(dO O) inherits O's P rounding), P^T dO
+    leaves 5.4e-2 in dV of a corrupted block whose queries put P near 1 on one
+    amplified key, and bf16 outputs add O's output rounding to D (about 0.1 in
+    dQ)."""
+    joint_check(WORKLOADS["128k"], 0, n_random=8, hilo=bd.HILO_ALL)
 
 
 def test_workload_128k_block_reading():
-    joint_check(WORKLOADS["128k"], 1, n_random=4, hilo=bd.HILO_PV | bd.HILO_DQ)
+    joint_check(WORKLOADS["128k"], 1, n_random=4, hilo=bd.HILO_ALL)
 
 
 def csbp_ranges(w):
