@@ -212,6 +212,29 @@ bdlm_status bdlm_attn_bwd(const bdlm_problem* p,
                           void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * bdlm_attn_bwd without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same arguments, arithmetic, kernels and results as
+ * bdlm_attn_bwd; D and LSE * log2(e) live in a library-owned device array of
+ * BDLM_NOALLOC_SCRATCH_BYTES bytes instead (one per GPU, held until the process
+ * ends).  The call allocates nothing.  Query ranges that need more than the
+ * array holds (bdlm_attn_bwd_workspace_bytes() > BDLM_NOALLOC_SCRATCH_BYTES,
+ * i.e. more than about 8M (batch x row x head) entries) are rejected with
+ * BDLM_ERR_UNSUPPORTED before anything is enqueued.  The array of the device
+ * current at the call is used, so `stream` must belong to that device.  Every
+ * call on one GPU shares its array: calls that overlap in time on one GPU
+ * (other streams, other threads) race and must be serialised by the caller.
+ */
+#define BDLM_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+bdlm_status bdlm_attn_bwd_noalloc(const bdlm_problem* p,
+                                  int32_t n_q, const bdlm_range* q_ranges,
+                                  const void* const* q, const void* const* o, const float* const* lse,
+                                  const void* const* dO, void* const* dq,
+                                  int32_t n_k, const bdlm_range* k_ranges,
+                                  const void* const* k, const void* const* v,
+                                  void* const* dk, void* const* dv, hipStream_t stream);
+
+/*
  * Number of valid query-key pairs of the mask per (batch element, query head),
  * summed over the given ranges (the paper's unit of attention work, App. B
  * eq:block-work-by-position).  Host only; returns -1 on invalid arguments.

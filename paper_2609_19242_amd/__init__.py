@@ -24,7 +24,7 @@ __all__ = [
     "BF16", "F32", "CLEAN", "CORRUPTED", "CLEAN_INTRA_CAUSAL", "CLEAN_INTRA_BLOCK",
     "HILO_PV", "HILO_DKDV", "HILO_DQ", "HILO_ALL",
     "make_problem", "joint_ranges", "attn_fwd", "attn_partial_fwd", "lse_merge",
-    "attn_bwd_workspace_bytes", "attn_bwd", "visible_pairs",
+    "attn_bwd_workspace_bytes", "attn_bwd", "attn_bwd_noalloc", "visible_pairs",
     "joint_fwd", "joint_bwd", "timing_enable", "timing_collect", "useful_flops",
 ]
 
@@ -35,6 +35,7 @@ CLEAN_INTRA_CAUSAL, CLEAN_INTRA_BLOCK = 0, 1
 HILO_PV, HILO_DKDV, HILO_DQ = 1, 2, 4
 HILO_ALL = HILO_PV | HILO_DKDV | HILO_DQ
 MAX_Q_RANGES, MAX_K_RANGES, MAX_MERGE_PARTS = 4, 32, 32
+NOALLOC_SCRATCH_BYTES = 64 << 20  # BDLM_NOALLOC_SCRATCH_BYTES
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 # BDLM_LIBRARY points the binding at another build of the same C ABI (e.g. a
@@ -96,6 +97,9 @@ def lib() -> ctypes.CDLL:
         L.bdlm_attn_bwd.argtypes = [ctypes.POINTER(Problem), ctypes.c_int32, ctypes.POINTER(Range), _PP, _PP, _PP,
                                     _PP, _PP, ctypes.c_int32, ctypes.POINTER(Range), _PP, _PP, _PP, _PP,
                                     _VP, ctypes.c_size_t, _VP]
+        L.bdlm_attn_bwd_noalloc.argtypes = [ctypes.POINTER(Problem), ctypes.c_int32, ctypes.POINTER(Range), _PP, _PP,
+                                             _PP, _PP, _PP, ctypes.c_int32, ctypes.POINTER(Range), _PP, _PP, _PP, _PP,
+                                             _VP]
         L.bdlm_visible_pairs.argtypes = [ctypes.POINTER(Problem), ctypes.c_int32, ctypes.POINTER(Range),
                                          ctypes.c_int32, ctypes.POINTER(Range)]
         L.bdlm_visible_pairs.restype = ctypes.c_int64
@@ -105,7 +109,8 @@ def lib() -> ctypes.CDLL:
         L.bdlm_timing_collect.restype = ctypes.c_int32
         L.bdlm_kernel_name.argtypes = [ctypes.c_int32]
         L.bdlm_kernel_name.restype = ctypes.c_char_p
-        for name in ("bdlm_attn_fwd", "bdlm_attn_partial_fwd", "bdlm_lse_merge", "bdlm_attn_bwd"):
+        for name in ("bdlm_attn_fwd", "bdlm_attn_partial_fwd", "bdlm_lse_merge", "bdlm_attn_bwd",
+                     "bdlm_attn_bwd_noalloc"):
             getattr(L, name).restype = ctypes.c_int
         _LIB = L
     return _LIB
@@ -221,6 +226,14 @@ def attn_bwd(p: Problem, q_ranges, q, o, lse, dO, dq, k_ranges, k, v, dk, dv, wo
     _check(lib().bdlm_attn_bwd(ctypes.byref(p), len(q_ranges), _rarr(q_ranges), _parr(q), _parr(o), _parr(lse),
                                _parr(dO), _parr(dq), len(k_ranges), _rarr(k_ranges), _parr(k), _parr(v),
                                _parr(dk), _parr(dv), _ptr(workspace), nbytes, _stream(stream)))
+
+
+def attn_bwd_noalloc(p: Problem, q_ranges, q, o, lse, dO, dq, k_ranges, k, v, dk, dv, stream=None):
+    """``bdlm_attn_bwd_noalloc``: :func:`attn_bwd` without a workspace (the library's per-GPU scratch
+    array of ``NOALLOC_SCRATCH_BYTES`` holds D); calls that overlap on one GPU race."""
+    _check(lib().bdlm_attn_bwd_noalloc(ctypes.byref(p), len(q_ranges), _rarr(q_ranges), _parr(q), _parr(o),
+                                       _parr(lse), _parr(dO), _parr(dq), len(k_ranges), _rarr(k_ranges), _parr(k),
+                                       _parr(v), _parr(dk), _parr(dv), _stream(stream)))
 
 
 def visible_pairs(p: Problem, q_ranges: Sequence[Range], k_ranges: Sequence[Range]) -> int:

@@ -7,6 +7,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -307,11 +308,44 @@ size_t bdlm_attn_bwd_workspace_bytes(const bdlm_problem* p, int32_t n_q, const b
   return tot;
 }
 
-bdlm_status bdlm_attn_bwd(const bdlm_problem* p, int32_t n_q, const bdlm_range* q_ranges, const void* const* q,
+}  // extern "C"
+
+namespace {
+
+// ---- the allocation-free backward's workspace: a file-scope device array.
+// Each GPU the library runs on holds its own copy until the process ends; its
+// address on the current device is looked up once per device and kept.
+constexpr size_t kScratchBytes = BDLM_NOALLOC_SCRATCH_BYTES;
+constexpr int kMaxDevices = 64;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+bdlm_status scratch_of_current_device(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(BDLM_ERR_UNSUPPORTED, "device %d: the scratch table holds %d devices", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return BDLM_OK;
+}
+
+// The backward with its D / LSE*log2(e) arrays in `workspace`, or (workspace
+// == nullptr and use_scratch) in the current device's scratch array.  Every
+// argument is validated before the first HIP call.
+bdlm_status attn_bwd_impl(const bdlm_problem* p, int32_t n_q, const bdlm_range* q_ranges, const void* const* q,
                           const void* const* o, const float* const* lse, const void* const* dO, void* const* dq,
                           int32_t n_k, const bdlm_range* k_ranges, const void* const* k, const void* const* v,
                           void* const* dk, void* const* dv, void* workspace, size_t workspace_bytes,
-                          hipStream_t stream) {
+                          bool use_scratch, hipStream_t stream) {
   bdlm_status st;
   if ((st = check_problem(p)) != BDLM_OK) return st;
   if ((st = check_counts(n_q, n_k, q_ranges, k_ranges)) != BDLM_OK) return st;
@@ -319,14 +353,22 @@ bdlm_status bdlm_attn_bwd(const bdlm_problem* p, int32_t n_q, const bdlm_range* 
   for (int i = 0; i < n_q; ++i)
     if ((st = check_range(p, q_ranges[i], "query", i)) != BDLM_OK) return st;
   const size_t need = bdlm_attn_bwd_workspace_bytes(p, n_q, q_ranges);
-  if (need > 0 && (!workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255u)))
+  if (use_scratch) {
+    if (need > kScratchBytes)
+      return fail(BDLM_ERR_UNSUPPORTED,
+                  "the allocation-free backward needs %zu bytes of scratch for these query ranges; its limit is %zu "
+                  "(2 x batch x rows x heads fp32 values per query range, each array rounded up to 256 bytes)",
+                  need, kScratchBytes);
+  } else if (need > 0 && (!workspace || workspace_bytes < need || (reinterpret_cast<uintptr_t>(workspace) & 255u))) {
     return fail(BDLM_ERR_WORKSPACE, "workspace needs %zu bytes, 256-byte aligned (got %zu at %p)", need,
                 workspace_bytes, workspace);
+  }
   AttnArgs a;
   fill_common(a, p);
   a.n_q = n_q;
   a.n_k = n_k;
-  char* ws = static_cast<char*>(workspace);
+  size_t ws_off[kMaxQ] = {};
+  size_t off = 0;
   for (int i = 0; i < n_q; ++i) {
     const bdlm_range& r = q_ranges[i];
     if (r.len > 0) {
@@ -347,9 +389,8 @@ bdlm_status bdlm_attn_bwd(const bdlm_problem* p, int32_t n_q, const bdlm_range* 
     if (arr > ((size_t)1 << 30))
       return fail(BDLM_ERR_UNSUPPORTED, "query range %d: batch * len * heads = %zu rows exceeds 2^28", i,
                   rows * p->heads);
-    a.qr[i].l2 = reinterpret_cast<float*>(ws);
-    a.qr[i].delta = reinterpret_cast<float*>(ws + arr);
-    ws += 2 * arr;
+    ws_off[i] = off;  // l2 at off, D at off + arr (pointers set once the base is known)
+    off += 2 * arr;
   }
   for (int j = 0; j < n_k; ++j) {
     if ((st = check_range(p, k_ranges[j], "key", j)) != BDLM_OK) return st;
@@ -369,6 +410,30 @@ bdlm_status bdlm_attn_bwd(const bdlm_problem* p, int32_t n_q, const bdlm_range* 
   const int64_t tiles = tile_ranges(a.kr, n_k, keys);
   if ((st = check_grid(tiles, (int64_t)p->kv_heads * p->batch)) != BDLM_OK) return st;
   a.total_tiles = (int32_t)tiles;
+  // The dQ kernel walks query tiles of the forward's height.
+  AttnArgs aq = a;
+  if (p->dtype == BDLM_BF16) {
+    const int64_t qt = tile_ranges(aq.qr, n_q, kFwdRowsBf16);
+    if ((st = check_grid(qt, (int64_t)p->heads * p->batch)) != BDLM_OK) return st;
+    aq.total_tiles = (int32_t)qt;
+    aq.interleave = 1;
+    for (int i = 1; i < n_q; ++i)
+      if (aq.qr[i].ntiles != aq.qr[0].ntiles) aq.interleave = 0;
+  }
+  // Validation done: place D and LSE*log2(e).
+  char* base = static_cast<char*>(workspace);
+  if (use_scratch && need > 0) {
+    void* sp = nullptr;
+    if ((st = scratch_of_current_device(&sp)) != BDLM_OK) return st;
+    base = static_cast<char*>(sp);
+  }
+  for (int i = 0; i < n_q; ++i) {
+    const size_t arr = align256((size_t)p->batch * (size_t)q_ranges[i].len * p->heads * sizeof(float));
+    float* l2 = need > 0 ? reinterpret_cast<float*>(base + ws_off[i]) : nullptr;
+    float* dl = need > 0 ? reinterpret_cast<float*>(base + ws_off[i] + arr) : nullptr;
+    a.qr[i].l2 = aq.qr[i].l2 = l2;
+    a.qr[i].delta = aq.qr[i].delta = dl;
+  }
   // Visit key ranges heaviest first: clean ranges by ascending position (their
   // early keys are seen by the most queries), then corrupted ranges.
   int n = 0;
@@ -389,14 +454,7 @@ bdlm_status bdlm_attn_bwd(const bdlm_problem* p, int32_t n_q, const bdlm_range* 
   if (p->dtype == BDLM_BF16) {
     e = timed(kKBwdBf16, stream, [&] { return launch_bwd_bf16(a, p->head_dim, stream); });
     if (e != hipSuccess) return hip_fail(e, "backward dK/dV launch");
-    // The dQ kernel walks query tiles of the forward's height.
-    AttnArgs aq = a;
-    const int64_t qt = tile_ranges(aq.qr, n_q, kFwdRowsBf16);
-    if ((st = check_grid(qt, (int64_t)p->heads * p->batch)) != BDLM_OK) return st;
-    aq.total_tiles = (int32_t)qt;
-    aq.interleave = 1;
-    for (int i = 1; i < n_q; ++i)
-      if (aq.qr[i].ntiles != aq.qr[0].ntiles) aq.interleave = 0;
+    for (int j = 0; j < n_k; ++j) aq.order[j] = a.order[j];
     e = timed(kKBwdDq, stream, [&] { return launch_bwd_dq_bf16(aq, p->head_dim, stream); });
     if (e != hipSuccess) return hip_fail(e, "backward dQ launch");
   } else {
@@ -404,6 +462,27 @@ bdlm_status bdlm_attn_bwd(const bdlm_problem* p, int32_t n_q, const bdlm_range* 
     if (e != hipSuccess) return hip_fail(e, "backward launch");
   }
   return BDLM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+bdlm_status bdlm_attn_bwd(const bdlm_problem* p, int32_t n_q, const bdlm_range* q_ranges, const void* const* q,
+                          const void* const* o, const float* const* lse, const void* const* dO, void* const* dq,
+                          int32_t n_k, const bdlm_range* k_ranges, const void* const* k, const void* const* v,
+                          void* const* dk, void* const* dv, void* workspace, size_t workspace_bytes,
+                          hipStream_t stream) {
+  return attn_bwd_impl(p, n_q, q_ranges, q, o, lse, dO, dq, n_k, k_ranges, k, v, dk, dv, workspace,
+                       workspace_bytes, false, stream);
+}
+
+bdlm_status bdlm_attn_bwd_noalloc(const bdlm_problem* p, int32_t n_q, const bdlm_range* q_ranges,
+                                  const void* const* q, const void* const* o, const float* const* lse,
+                                  const void* const* dO, void* const* dq, int32_t n_k, const bdlm_range* k_ranges,
+                                  const void* const* k, const void* const* v, void* const* dk, void* const* dv,
+                                  hipStream_t stream) {
+  return attn_bwd_impl(p, n_q, q_ranges, q, o, lse, dO, dq, n_k, k_ranges, k, v, dk, dv, nullptr, 0, true, stream);
 }
 
 bdlm_status bdlm_timing_enable(int32_t on) {

@@ -215,3 +215,26 @@ def test_size_limits_rejected_before_launch():
     assert L.bdlm_lse_merge(1, 1 << 26, 32, 128, 1, parts, parts, 0, FAKE + 4096, FAKE + 8192, 0, None) == -2
     assert "2^31" in L.bdlm_last_error().decode()
     assert L.bdlm_lse_merge(1 << 40, 1 << 40, 1 << 30, 128, 1, parts, parts, 0, FAKE + 4096, FAKE + 8192, 0, None) == -2
+
+
+@host_only
+def test_noalloc_backward_rejects_scratch_overflow_before_launch():
+    """bdlm_attn_bwd_noalloc: query ranges whose D arrays exceed the library's scratch array
+    are rejected with BDLM_ERR_UNSUPPORTED before anything is enqueued."""
+    L = 1 << 20  # 2 ranges x 2 arrays x 2^20 rows x 16 heads x 4 bytes = 256 MiB > 64 MiB
+    p = _prob(L=L, block_size=64, heads=16, kv_heads=2)
+    r = bd.joint_ranges(L)
+    assert bd.attn_bwd_workspace_bytes(p, r) > bd.NOALLOC_SCRATCH_BYTES
+    fake = [FAKE, FAKE]
+    st = bd.lib().bdlm_attn_bwd_noalloc(ctypes.byref(p), 2, bd._rarr(r), bd._parr(fake), bd._parr(fake),
+                                        bd._parr(fake), bd._parr(fake), bd._parr(fake), 2, bd._rarr(r),
+                                        bd._parr(fake), bd._parr(fake), bd._parr(fake), bd._parr(fake), None)
+    assert st == -2
+    assert "scratch" in bd.lib().bdlm_last_error().decode()
+    # the same call on a problem that fits passes the size check and stops at the next validation step
+    p2 = _prob(L=64, block_size=16)
+    r2 = bd.joint_ranges(64)
+    st = bd.lib().bdlm_attn_bwd_noalloc(ctypes.byref(p2), 2, bd._rarr(r2), bd._parr(fake), bd._parr(fake),
+                                        bd._parr(fake), bd._parr(fake), bd._parr([FAKE + 8, FAKE]), 2, bd._rarr(r2),
+                                        bd._parr(fake), bd._parr(fake), bd._parr(fake), bd._parr(fake), None)
+    assert st == -1 and "aligned" in bd.lib().bdlm_last_error().decode()
