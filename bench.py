@@ -44,7 +44,7 @@ PEAK_HBM_GBS = 8000.0
 # trusted while these are unchanged).
 KERNEL_SOURCES = {
     "fwd_bf16": ["common.hpp", "device.hpp", "qtiles.hpp", "fwd_bf16.hip"],
-    "bwd_dkdv_bf16": ["common.hpp", "device.hpp", "bwd_bf16.hip"],
+    "bwd_dkdv_bf16": ["common.hpp", "device.hpp", "bwd_dkdv.hip"],
     "bwd_dq_bf16": ["common.hpp", "device.hpp", "qtiles.hpp", "bwd_dq.hip"],
 }
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_32k.json")

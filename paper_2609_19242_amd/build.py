@@ -17,7 +17,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libbdlm_attn.so")
 BUILD_DIR = os.path.join(HERE, "_build")
-SOURCES = ["api.cpp", "fwd_bf16.hip", "fwd_f32.hip", "merge.hip", "bwd_pre.hip", "bwd_bf16.hip", "bwd_dq.hip", "bwd_f32.hip"]
+SOURCES = ["api.cpp", "fwd_bf16.hip", "fwd_f32.hip", "merge.hip", "bwd_pre.hip", "bwd_bf16.hip", "bwd_dkdv.hip",
+           "bwd_dq.hip", "bwd_f32.hip"]
 ARCH = os.environ.get("BDLM_OFFLOAD_ARCH", "gfx950")
 # Per-source code-generation options.  The dK/dV kernel runs one wave per SIMD,
 # so its speed is its own instruction stream: the iterative ILP scheduler keeps
@@ -25,7 +26,10 @@ ARCH = os.environ.get("BDLM_OFFLOAD_ARCH", "gfx950")
 # sharing AGPRs between the per-step S/dP tiles and the dK/dV accumulators
 # (about 190 -> 70 register-file copies per step).  Measured at L=32768:
 # 44.4 -> 42.9 -> 38.9 ms; both are slower for the two-waves-per-SIMD kernels.
-EXTRA_FLAGS = {"bwd_bf16.hip": ["-mllvm", "-amdgpu-sched-strategy=iterative-ilp", "-mllvm", "-amdgpu-mfma-vgpr-form"]}
+EXTRA_FLAGS = {"bwd_bf16.hip": ["-mllvm", "-amdgpu-sched-strategy=iterative-ilp", "-mllvm", "-amdgpu-mfma-vgpr-form"],
+               # score and dP accumulators in VGPRs (the softmax reads them); the
+               # dK/dV accumulators are AGPR operands of inline-assembly MFMAs
+               "bwd_dkdv.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
 def hipcc() -> str:

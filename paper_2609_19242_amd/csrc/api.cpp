@@ -367,6 +367,9 @@ bdlm_status attn_bwd_impl(const bdlm_problem* p, int32_t n_q, const bdlm_range* 
   fill_common(a, p);
   a.n_q = n_q;
   a.n_k = n_k;
+  int n_q_rows = 0;  // query ranges with rows (empty ones add no work to dK/dV)
+  for (int i = 0; i < n_q; ++i) n_q_rows += q_ranges[i].len > 0 ? 1 : 0;
+  a.stats_form = dkdv_uses_scheduled_kernel(p->dtype == BDLM_BF16, p->head_dim, p->hilo, a.group, n_q_rows) ? 1 : 0;
   size_t ws_off[kMaxQ] = {};
   size_t off = 0;
   for (int i = 0; i < n_q; ++i) {
@@ -452,7 +455,16 @@ bdlm_status attn_bwd_impl(const bdlm_problem* p, int32_t n_q, const bdlm_range* 
   hipError_t e = timed(kKBwdPre, stream, [&] { return launch_bwd_pre(a, p->head_dim, p->dtype, stream); });
   if (e != hipSuccess) return hip_fail(e, "backward pre-pass launch");
   if (p->dtype == BDLM_BF16) {
-    e = timed(kKBwdBf16, stream, [&] { return launch_bwd_bf16(a, p->head_dim, stream); });
+    e = timed(kKBwdBf16, stream, [&] {
+      if (!a.stats_form) return launch_bwd_bf16(a, p->head_dim, stream);
+      // The scheduled kernel walks at most two query ranges: pass it the ranges
+      // that have rows, in call order (the order the walk accumulates in).
+      AttnArgs ak = a;
+      ak.n_q = 0;
+      for (int i = 0; i < n_q; ++i)
+        if (a.qr[i].len > 0) ak.qr[ak.n_q++] = a.qr[i];
+      return launch_bwd_dkdv(ak, stream);
+    });
     if (e != hipSuccess) return hip_fail(e, "backward dK/dV launch");
     for (int j = 0; j < n_k; ++j) aq.order[j] = a.order[j];
     e = timed(kKBwdDq, stream, [&] { return launch_bwd_dq_bf16(aq, p->head_dim, stream); });

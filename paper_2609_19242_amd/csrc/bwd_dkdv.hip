@@ -1,0 +1,569 @@
+// dK and dV of the BDLM attention backward, key-major, bf16 inputs, fp32
+// accumulation, head_dim 128, gfx950: the software-pipelined kernel.
+//
+// Exact gradients from the saved O and LSE (arXiv 2609.19242 App. C fused
+// backward; eq:correctness-corrupted-gradient and eq:correctness-clean-gradient):
+// with P = exp(scale Q K^T + mask - LSE) and D = rowsum(dO * O),
+//   dV = P^T dO,  dS = P * (dO V^T - D),  dK = scale dS^T Q,
+// summed over every query row that sees a key and over the query heads of the
+// key's GQA group.  dQ comes from the query-major kernel (bwd_dq.hip).
+//
+// Work split as in bwd_bf16.hip: a workgroup owns 128 keys of one KV head (4
+// waves x 32 keys, one wave per SIMD), holds their K and V rows in AGPRs as
+// MFMA operands and accumulates dK^T and dV^T in AGPRs over the whole walk of
+// visible 32-row query steps (every query range, two query heads per step).
+//
+// What differs is the schedule of a step.  With one wave per SIMD nothing
+// hides a wave's own dependency chain S, dP -> softmax -> dV, dK, so the step
+// is written as four blocks of 16 matrix products each, with the vector and
+// scalar work placed under them and the order fixed by scheduling fences:
+//   A: S_0 = Q_0 K^T, dP_0 = dO_0 V^T (head 0)  under  the LDS-DMA copies of
+//      the step three ahead, the walk's next position and its copy plan
+//   B: S_1, dP_1 (head 1)      under  P_0 = exp2(c S_0), dS_0 = P_0 dP_0
+//   C: dV += dO_0^T P_0, dK += Q_0^T dS_0   under  P_1 = exp2(c S_1)
+//   D: dV += dO_1^T P_1, dK += Q_1^T dS_1   under  dS_1 = P_1 dP_1, and the
+//      next step's accumulator starts
+// Every product's LDS operand is read four products ahead.  The walk is
+// branch-free, and empty asm statements pin its scalar work to its place in
+// the order (the compiler would otherwise hoist it to the top of the step,
+// where nothing overlaps it).
+// S and dP accumulate on top of -LSE/scale and -D read from LDS (the pre-pass
+// writes that form), so the softmax is one multiply and one exp2 per score
+// and dS one multiply; rows the mask hides start at -inf.  LDS holds four
+// stages, filled by LDS-DMA copies three steps ahead, so the next step's
+// data is resident while a step runs; the copies are issued as inline
+// assembly, which keeps the compiler from waiting on them before every LDS
+// transpose read (it cannot tell which stage a DMA writes).  The dV/dK
+// products are inline-assembly MFMAs on AGPR accumulators (the S/dP products
+// use VGPR accumulators, which the softmax reads).
+#include "common.hpp"
+#include "device.hpp"
+
+namespace bdlm {
+
+namespace {
+
+constexpr int kD = 128;                 // head_dim
+constexpr int kKS = kD / 16;            // k-steps of 16 in a score product
+constexpr int kDT = kD / 32;            // 32-wide d tiles of dK^T / dV^T
+constexpr int kBM = 32;                 // query rows per step
+constexpr int kNH = 2;                  // query heads per step
+constexpr int kStages = 4;
+constexpr uint32_t kRB = kD * 2;        // bytes per row
+constexpr uint32_t kHB = kBM * kRB;     // bytes per head in a stage tile (8 KB)
+constexpr uint32_t kTileB = kNH * kHB;  // Q (or dO) tile of a stage (16 KB)
+// LDS: the four Q tiles, then the four dO tiles (each region 64 KB, so every
+// read address is a per-lane register plus an immediate offset below 2^16),
+// then per stage -LSE/scale and -D of the step's 2 x 32 rows.
+constexpr uint32_t kQRegion = 0;
+constexpr uint32_t kDoRegion = kStages * kTileB;                 // 65536
+constexpr uint32_t kStatRegion = 2 * kStages * kTileB;           // 131072
+constexpr uint32_t kStatB = 2 * kNH * kBM * 4;                   // 512 bytes per stage
+constexpr uint32_t kSpareRegion = kStatRegion + kStages * kStatB; // empty copies of waves 0, 1
+constexpr uint32_t kLdsBytes = kSpareRegion + 2 * 256;             // 133632
+// Copy plan: a tensor tile of a step is 2 heads x 32 rows x 16 chunks = 1024
+// 16-byte slots = 16 instructions of 64 lanes; waves 0-1 copy Q, waves 2-3 dO,
+// 8 instructions each; one more dword instruction per wave copies the 64
+// floats of -LSE/scale (wave 2) or -D (wave 3) (waves 0, 1: an empty copy).
+constexpr int kIPW = 8;
+
+__device__ __forceinline__ void mfma_agpr(f32x16& acc, const bf16x8& a, const bf16x8& b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
+
+// Buffer resource as four SGPRs for the inline-assembly copies.
+__device__ __forceinline__ u32x4 rsrc_words(const void* base, uint32_t bytes) {
+  const uint64_t p = (uint64_t)(uintptr_t)base;
+  u32x4 r;
+  r[0] = (uint32_t)p;
+  r[1] = (uint32_t)(p >> 32) & 0xffffu;
+  r[2] = bytes;
+  r[3] = 0x00020000u;
+  return r;
+}
+// Global -> LDS copy: lane i's 16 (or 4) bytes at voff land at LDS byte
+// address m0 + 16 i (4 i); offsets past the resource's end write zeros.
+__device__ __forceinline__ void dma16(u32x4 rsrc, uint32_t lds_byte, uint32_t voff) {
+  asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds" ::"v"(voff), "s"(rsrc), "{m0}"(lds_byte)
+               : "memory");
+}
+__device__ __forceinline__ void dma4(u32x4 rsrc, uint32_t lds_byte, uint32_t voff) {
+  asm volatile("s_nop 0\n\tbuffer_load_dword %0, %1, 0 offen lds" ::"v"(voff), "s"(rsrc), "{m0}"(lds_byte)
+               : "memory");
+}
+
+__device__ __forceinline__ void fence() { __builtin_amdgcn_sched_barrier(0); }
+
+__device__ __forceinline__ f32x4 lds_f4(uint32_t a) {
+  return *(__attribute__((address_space(3))) const f32x4*)(uintptr_t)a;
+}
+
+__global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
+  constexpr int BN = kBwdKeysBf16, BM = kBM, NH = kNH;
+  static_assert(BN == 128, "tile shape");
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[kLdsBytes];
+  const uint32_t L0 = lds_addr(lds);
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l32 = lane & 31, half = lane >> 5;
+  const int G = lane >> 4, sl = lane & 15;
+  const int64_t H = a.heads, HKV = a.kv_heads;
+
+  // ---- work item: (batch, KV head, key range, key tile); heaviest tiles first per XCD
+  const int T = a.total_tiles;
+  const int logical = xcd_remap(blockIdx.x, T * a.kv_heads * a.batch);
+  const int bk = logical / T;
+  int order = logical - bk * T;
+  const int b = bk / a.kv_heads, kvh = bk - (bk / a.kv_heads) * a.kv_heads;
+  int r = a.order[0], t = order;
+  for (int n = 0; n < a.n_k; ++n) {
+    const int rr = a.order[n];
+    const int nt = a.kr[rr].ntiles;
+    if (order < nt) {
+      r = rr;
+      t = order;
+      break;
+    }
+    order -= nt;
+  }
+  const KRangeArg& kr = a.kr[r];
+  const int key0 = t * BN;
+  const int nk = imin(BN, kr.len - key0);
+  const bool ragged = nk < BN;
+  const int mykey = w * 32 + l32;
+  const bool key_ok = mykey < nk;
+  const int pk = kr.pos0 + key0 + imin(mykey, nk - 1);
+  const int kpos_first = kr.pos0 + key0, kpos_last = kr.pos0 + key0 + nk - 1;
+
+  // ---- K, V rows of this wave's keys (B operands of the score products), in AGPRs
+  bf16x8 kf[kKS], vf[kKS];
+  {
+    const int64_t eoff = (((int64_t)b * kr.bstride + key0) * HKV + kvh) * kD;
+    const uint32_t bytes = (uint32_t)(((int64_t)(nk - 1) * HKV * kD + kD) * 2);
+    const auto rk = make_rsrc((const bf16*)kr.k + eoff, bytes);
+    const auto rv = make_rsrc((const bf16*)kr.v + eoff, bytes);
+    const uint32_t off = (uint32_t)(((int64_t)mykey * HKV * kD + 8 * half) * 2);
+#pragma unroll
+    for (int s = 0; s < kKS; ++s) {
+      kf[s] = __builtin_bit_cast(bf16x8, buf_load16(rk, off + 32 * s));
+      vf[s] = __builtin_bit_cast(bf16x8, buf_load16(rv, off + 32 * s));
+    }
+#pragma unroll
+    for (int s = 0; s < kKS; ++s) asm volatile("" : "+a"(kf[s]), "+a"(vf[s]));
+  }
+  // dK^T / dV^T accumulators (AGPRs, written only by the inline-assembly MFMAs)
+  f32x16 dka[kDT], dva[kDT];
+#pragma unroll
+  for (int d = 0; d < kDT; ++d) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      dka[d][i] = 0.f;
+      dva[d][i] = 0.f;
+    }
+    asm volatile("" : "+a"(dka[d]), "+a"(dva[d]));
+  }
+
+  // ---- walk over (query range, head pair, step), steps from the end of the
+  // ranges down (every range active at a step index, then the next index);
+  // the call passes at most two query ranges (the ones with rows).
+  struct Span {
+    int s0, s1, f0, f1, pos0, qa, qw, len;
+    const bf16* tb;
+    const float* lb;
+    uint32_t lrec;
+  };
+  auto make_span = [&](int q) -> Span {
+    Span sp{0, 0, 0, 0, 0, 0, 0, 0, nullptr, nullptr, 0u};
+    if (q >= a.n_q) return sp;
+    const QRangeArg& qr = a.qr[q];
+    sp.pos0 = qr.pos0;
+    sp.len = qr.len;
+    const int h0 = kvh * a.group;
+    sp.tb = (const bf16*)(w < 2 ? qr.q : qr.dO) + ((int64_t)b * qr.bstride * H + h0) * kD;
+    const int64_t lrow = ((int64_t)b * H + h0) * qr.len;
+    sp.lb = (w == 2 ? qr.l2 : qr.delta) + lrow;
+    sp.lrec = (uint32_t)(((int64_t)a.batch * H * qr.len - lrow) * 4);
+    int lo0, hi0, lo1, hi1;
+    query_interval(qr.stream, kr.stream, kpos_first, rule_of(a), lo0, hi0);
+    query_interval(qr.stream, kr.stream, kpos_last, rule_of(a), lo1, hi1);
+    const int u0 = imax(lo0 - qr.pos0, 0), u1 = imin(hi1 - qr.pos0, qr.len);
+    if (u1 > u0) {
+      sp.s0 = u0 / BM;
+      sp.s1 = (u1 + BM - 1) / BM;
+      const int i0 = imax(lo1 - qr.pos0, 0), i1 = imin(hi0 - qr.pos0, qr.len);
+      if (i1 > i0 && !ragged) {
+        sp.f0 = (i0 + BM - 1) / BM;
+        sp.f1 = i1 / BM;
+      }
+    }
+    int lo, hi;
+    query_interval(qr.stream, kr.stream, pk, rule_of(a), lo, hi);
+    lo = imax(lo, qr.pos0);
+    hi = imin(hi, qr.pos0 + qr.len);
+    sp.qa = lo;
+    sp.qw = key_ok ? imax(hi - lo, 0) : 0;
+    return sp;
+  };
+  const Span R0 = make_span(0), R1 = make_span(1);
+  auto sel2 = [](int q, auto v0, auto v1) { return q ? v1 : v0; };
+#define BDLM_PICK(f, q) sel2((q), R0.f, R1.f)
+  auto active = [](const Span& sp, int s) { return sp.s0 <= s && s < sp.s1; };
+  auto below = [](const Span& sp, int s) {
+    const int cand = imin(s - 1, sp.s1 - 1);
+    return cand >= sp.s0 ? cand : -1;
+  };
+  struct Cursor {
+    int q, hp, s;
+  };
+  const int npairs = a.group / NH;
+  // Next (range, head pair, step) of the walk, as selects only (no branches,
+  // so the compiler can place it between the products of a step).
+  auto advance = [&](Cursor c) __attribute__((always_inline)) -> Cursor {
+    const bool live = c.s >= 0;
+    const bool wrap = c.hp + 1 >= npairs;
+    const bool next_range = c.q == 0 && active(R1, c.s);  // the other range at the same step
+    const int s_next = imax(below(R0, c.s), below(R1, c.s));
+    const int q_first = active(R0, s_next) ? 0 : 1;
+    Cursor n;
+    n.hp = wrap ? 0 : c.hp + 1;
+    n.q = !wrap ? c.q : next_range ? 1 : (s_next >= 0 ? q_first : 0);
+    n.s = (!wrap || next_range) ? c.s : s_next;
+    return live ? n : c;
+  };
+
+  // ---- copies.  Instruction i of a wave is instruction (w & 1) * kIPW + i of
+  // its tensor; the per-lane global offsets are constant over the walk.
+  const int wodd = w & 1;
+  uint32_t voff[kIPW];
+#pragma unroll
+  for (int i = 0; i < kIPW; ++i) {
+    const int slot = (wodd * kIPW + i) * 64 + lane;
+    const int row = slot / 16, ch = (slot % 16) ^ chunk_swz<kD>(row);
+    const int j = row / BM, rr = row % BM;
+    voff[i] = (uint32_t)(((rr * H + j) * kD + ch * 8) * 2);
+  }
+  // A step's copies: kIPW 16-byte instructions of the wave's tensor and one
+  // dword instruction of -LSE/scale (wave 2) or -D (wave 3); waves 0 and 1
+  // issue an empty dword copy into a spare LDS row instead, so that every wave
+  // has kIPW + 1 copies per step in flight.
+  struct CopyPlan {
+    u32x4 rt, rl;   // resources: the wave's tensor rows, its -LSE/scale or -D row
+    uint32_t lvo;   // per-lane offset of the dword copy
+  };
+  // The copy resources of step c (selects only).
+  auto copy_plan = [&](const Cursor c) __attribute__((always_inline)) -> CopyPlan {
+    const bool live = c.s >= 0;
+    const int q = live ? c.q : 0;
+    const int row0 = live ? c.s * BM : 0;
+    const int len = BDLM_PICK(len, q);
+    const int nrows = imin(BM, len - row0);
+    const int hoff = c.hp * NH;
+    const uint32_t bytes = live ? (uint32_t)((nrows - 1) * (int)H + NH) * kD * 2 : 0u;
+    CopyPlan cp;
+    cp.rt = rsrc_words(BDLM_PICK(tb, q) + ((int64_t)row0 * H + hoff) * kD, bytes);
+    const int loff = hoff * len + row0;
+    const uint32_t lbytes = (live && w >= 2) ? BDLM_PICK(lrec, q) - (uint32_t)loff * 4u : 0u;
+    cp.rl = rsrc_words(BDLM_PICK(lb, q) + loff, lbytes);
+    cp.lvo = (uint32_t)(((lane >> 5) * len + (lane & 31)) * 4);
+    return cp;
+  };
+  auto copy_issue = [&](const CopyPlan& cp, int st, int i) __attribute__((always_inline)) {
+    if (i < kIPW) {
+      dma16(cp.rt, L0 + (w < 2 ? kQRegion : kDoRegion) + st * kTileB + (wodd * kIPW + i) * 1024, voff[i]);
+    } else {
+      const uint32_t ldst =
+          w >= 2 ? L0 + kStatRegion + st * kStatB + (w == 2 ? 0u : 256u) : L0 + kSpareRegion + w * 256;
+      dma4(cp.rl, ldst, cp.lvo);
+    }
+  };
+  auto copy_step = [&](int st, const Cursor c) __attribute__((always_inline)) {
+    const CopyPlan cp = copy_plan(c);
+#pragma unroll
+    for (int i = 0; i <= kIPW; ++i) copy_issue(cp, st, i);
+  };
+  // Pins scalar walk values at a point of the step's instruction order: an
+  // empty asm statement the values pass through (in) or must exist at (use).
+  auto pin_in = [](Cursor& c) __attribute__((always_inline)) {
+    asm volatile("" : "+s"(c.s), "+s"(c.q), "+s"(c.hp));
+  };
+  auto pin_use = [](const Cursor& c) __attribute__((always_inline)) {
+    asm volatile("" ::"s"(c.s), "s"(c.q), "s"(c.hp));
+  };
+
+  const float c = a.scale_log2;
+  // Per-lane read addresses (loop-invariant; stage, head and tensor are immediate offsets).
+  // Row reads: lane (half, l32) reads logical chunk 2k + half of row l32.
+  // (The dO addresses are laundered through an empty asm statement: otherwise
+  // the compiler re-derives them from the Q addresses with an add per read.)
+  uint32_t yq[kKS], yd[kKS];
+#pragma unroll
+  for (int k = 0; k < kKS; ++k) {
+    yq[k] = (L0 + kQRegion + swz_row_part<kD>(l32, half)) ^ (32u * k);
+    yd[k] = yq[k] + kDoRegion;
+    asm volatile("" : "+v"(yd[k]));
+  }
+  // Transpose reads: rows 16u + R0 and 16u + R0 + 8 of the head's tile, 8-byte
+  // piece 8d + 4 (G & 1) + (sl & 3).
+  uint32_t tq0[kDT], tq1[kDT], td0[kDT], td1[kDT];
+#pragma unroll
+  for (int d = 0; d < kDT; ++d) {
+    tq0[d] = (L0 + kQRegion + swz_tr_part<kD>(G, sl, 0)) ^ (64u * d);
+    tq1[d] = (L0 + kQRegion + swz_tr_part<kD>(G, sl, 8)) ^ (64u * d);
+    td0[d] = tq0[d] + kDoRegion;
+    td1[d] = tq1[d] + kDoRegion;
+    asm volatile("" : "+v"(td0[d]), "+v"(td1[d]));
+  }
+  // Accumulator starts of a step: for head j, register i of a lane holds query
+  // row 8 (i / 4) + 4 half + i % 4 of the step.
+  uint32_t ystat = L0 + kStatRegion + (uint32_t)(4 * half) * 4;
+  asm volatile("" : "+v"(ystat));  // one base register; stage, head and row offsets stay immediate
+
+  f32x16 sa[NH], da[NH];
+  // Load the starts of step `cu` (stage st) and apply the mask of partly visible steps.
+  auto load_starts = [&](int st, const Cursor cu) __attribute__((always_inline)) {
+    const uint32_t base = ystat + st * kStatB;
+#pragma unroll
+    for (int j = 0; j < NH; ++j)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const f32x4 l = lds_f4(base + (j * BM + 8 * g4) * 4);
+        const f32x4 dd = lds_f4(base + 256 + (j * BM + 8 * g4) * 4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          sa[j][4 * g4 + e] = l[e];
+          da[j][4 * g4 + e] = dd[e];
+        }
+      }
+    const int q = cu.s >= 0 ? cu.q : 0;
+    // Partly visible steps: hidden scores start at -inf.  The compare and the
+    // selects are inline assembly inside a wave-uniform branch: as plain code
+    // the compiler speculates them onto every step.
+    const int partial =
+        __builtin_amdgcn_readfirstlane((cu.s >= BDLM_PICK(f0, q) && cu.s < BDLM_PICK(f1, q)) ? 0 : 1);
+    if (partial) {
+      const int mbase = BDLM_PICK(pos0, q) + cu.s * BM + 4 * half - BDLM_PICK(qa, q);
+      const int lane_qw = BDLM_PICK(qw, q);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        float x0 = sa[0][i], x1 = sa[1][i];
+        uint32_t tmp;
+        // hidden when (unsigned)(mbase + row offset of register i) >= lane_qw
+        asm volatile(
+            "v_add_u32 %2, %3, %4\n\t"
+            "v_cmp_lt_u32 vcc, %2, %5\n\t"
+            "v_mov_b32 %2, 0xff800000\n\t"
+            "v_cndmask_b32 %0, %2, %0, vcc\n\t"
+            "v_cndmask_b32 %1, %2, %1, vcc"
+            : "+v"(x0), "+v"(x1), "=&v"(tmp)
+            : "n"(8 * (i >> 2) + (i & 3)), "v"(mbase), "v"(lane_qw)
+            : "vcc");
+        sa[0][i] = x0;
+        sa[1][i] = x1;
+      }
+    }
+  };
+
+  // One step on stage ST: the copies of step `cp` into stage CP go out under
+  // its first products, the starts of step `nx` (stage NX) are loaded under its
+  // last ones, and the walk advances under the softmax of head 0.
+  constexpr int RA = 4;  // row-read pairs in flight ahead of the score products
+  constexpr int TA = 4;  // transpose-read pairs in flight ahead of the dV/dK products
+  Cursor c0, c1, c2, c3;
+  CopyPlan cpl;  // copies of step c3, planned during the step before
+  auto run_step = [&](auto st_c, auto nx_c, int cp_stage) __attribute__((always_inline)) {
+    constexpr int ST = decltype(st_c)::value, NX = decltype(nx_c)::value;
+    constexpr uint32_t SO = ST * kTileB;  // stage offset inside a tensor region
+    // ---- A and B: S_j = Q_j K^T + start, dP_j = dO_j V^T + start, j = 0, 1 (32
+    // products), the softmax of head 0 under the products of head 1.
+    bf16x8 rq[RA + 1], rd[RA + 1];
+    auto rowq = [&](int n) { return lds_load16(yq[n % kKS] + SO + (n / kKS) * kHB); };
+    auto rowd = [&](int n) { return lds_load16(yd[n % kKS] + SO + (n / kKS) * kHB); };
+#pragma unroll
+    for (int n = 0; n < RA; ++n) {
+      rq[n] = rowq(n);
+      rd[n] = rowd(n);
+    }
+    fence();
+    bf16x8 pb[NH][2], dsb[NH][2];
+    Cursor c4;
+#pragma unroll
+    for (int n = 0; n < 2 * kKS; ++n) {
+      if (n + RA < 2 * kKS) {
+        rq[(n + RA) % (RA + 1)] = rowq(n + RA);
+        rd[(n + RA) % (RA + 1)] = rowd(n + RA);
+      }
+      const int j = n / kKS, k = n % kKS;
+      sa[j] = mfma32(rq[n % (RA + 1)], kf[k], sa[j]);
+      da[j] = mfma32(rd[n % (RA + 1)], vf[k], da[j]);
+      if (n <= kIPW) copy_issue(cpl, cp_stage, n);
+      if (n == kIPW + 1) {
+        pin_in(c3);
+        c4 = advance(c3);
+      }
+      if (n == kIPW + 2) pin_use(c4);
+      if (n == kIPW + 3) cpl = copy_plan(c4);
+      if (n == kIPW + 4) asm volatile("" ::"s"(cpl.rt), "s"(cpl.rl), "v"(cpl.lvo));
+
+      if (j == 1) {
+        // softmax of head 0: two scores per product pair
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const int i = 2 * k + e;
+          const float p = exp2f_fast(sa[0][i] * c);
+          da[0][i] = p * da[0][i];
+          sa[0][i] = p;
+        }
+        if (k & 1) {
+          const int i0 = 2 * (k - 1);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            pb[0][(i0 + e) >> 3][(i0 + e) & 7] = to_bf16(sa[0][i0 + e]);
+            dsb[0][(i0 + e) >> 3][(i0 + e) & 7] = to_bf16(da[0][i0 + e]);
+          }
+        }
+      }
+      fence();
+    }
+    // ---- C and D: dV^T += dO_j^T P_j, dK^T += Q_j^T dS_j (queries are the
+    // contraction index), head 0 under the softmax of head 1, head 1 under
+    // dS_1 and the next step's starts.  Per product: two transpose reads.
+    auto trd = [&](int j, int u, int d) {
+      const uint32_t o = SO + j * kHB + u * 16 * kRB;
+      return cat(lds_read_tr_at(td0[d] + o), lds_read_tr_at(td1[d] + o));
+    };
+    auto trq = [&](int j, int u, int d) {
+      const uint32_t o = SO + j * kHB + u * 16 * kRB;
+      return cat(lds_read_tr_at(tq0[d] + o), lds_read_tr_at(tq1[d] + o));
+    };
+    // product m of a head: m < 8 -> dV (u = m / 4, d = m % 4), else dK
+    auto opnd = [&](int j, int m) { return m < 8 ? trd(j, m / 4, m % 4) : trq(j, (m - 8) / 4, (m - 8) % 4); };
+    bf16x8 tf[TA + 1];
+#pragma unroll
+    for (int n = 0; n < TA; ++n) tf[n] = opnd(0, n);
+    fence();
+#pragma unroll
+    for (int n = 0; n < 32; ++n) {
+      if (n + TA < 32) tf[(n + TA) % (TA + 1)] = opnd((n + TA) / 16, (n + TA) % 16);
+      const int j = n / 16, m = n % 16;
+      if (m < 8) mfma_agpr(dva[m % 4], tf[n % (TA + 1)], pb[j][m / 4]);
+      else mfma_agpr(dka[(m - 8) % 4], tf[n % (TA + 1)], dsb[j][(m - 8) / 4]);
+      if (j == 0) {
+        // P_1 = exp2(c S_1): one score per product
+        sa[1][m] = exp2f_fast(sa[1][m] * c);
+        if (m & 1) {
+          pb[1][m >> 3][(m - 1) & 7] = to_bf16(sa[1][m - 1]);
+          pb[1][m >> 3][m & 7] = to_bf16(sa[1][m]);
+        }
+      } else if (m < 8) {
+        // dS_1 = P_1 dP_1 under the dV products of head 1
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const int i = 2 * m + e;
+          da[1][i] = sa[1][i] * da[1][i];
+        }
+        if (m & 1) {
+          const int i0 = 2 * (m - 1);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) dsb[1][(i0 + e) >> 3][(i0 + e) & 7] = to_bf16(da[1][i0 + e]);
+        }
+      } else if (m == 8) {
+        load_starts(NX, c1);
+      }
+      fence();
+    }
+    asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(kIPW + 1) : "memory");
+    c0 = c1;
+    c1 = c2;
+    c2 = c3;
+    c3 = c4;
+  };
+
+  // ---- the walk: four LDS stages, copies three steps ahead.  At the barrier
+  // closing step i every wave has waited for its copies of step i + 2 (only
+  // those of step i + 3 stay in flight) and has finished reading stage i,
+  // which the copies issued next overwrite.
+  c0.s = imax(below(R0, kBig), below(R1, kBig));
+  c0.q = (c0.s >= 0 && !active(R0, c0.s)) ? 1 : 0;
+  c0.hp = 0;
+  c1 = advance(c0);
+  c2 = advance(c1);
+  c3 = advance(c2);
+  cpl = copy_plan(c3);
+  copy_step(0, c0);
+  copy_step(1, c1);
+  copy_step(2, c2);
+  asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(kIPW + 1) : "memory");  // steps 0 and 1 landed
+  load_starts(0, c0);
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+  while (c0.s >= 0) {
+    run_step(I0{}, I1{}, 3);
+    if (c0.s < 0) break;
+    run_step(I1{}, I2{}, 0);
+    if (c0.s < 0) break;
+    run_step(I2{}, I3{}, 1);
+    if (c0.s < 0) break;
+    run_step(I3{}, I0{}, 2);
+  }
+  // Copies still in flight target stages nobody reads; they must land before
+  // the workgroup's LDS is released.  The last dV/dK products must finish
+  // before their accumulators are read.
+  asm volatile("s_waitcnt vmcnt(0)\n\ts_nop 15\n\ts_nop 15" ::: "memory");
+#undef BDLM_PICK
+
+  // ---- epilogue: dK = scale dK^T^T, dV (bf16 or fp32); unseen keys get zeros
+#pragma unroll
+  for (int d = 0; d < kDT; ++d) asm volatile("" : "+a"(dka[d]), "+a"(dva[d]));
+  if (key_ok) {
+    const int64_t off = (((int64_t)b * kr.bstride + key0 + mykey) * HKV + kvh) * kD;
+    if (a.out_f32) {
+      float* dkp = (float*)kr.dk + off;
+      float* dvp = (float*)kr.dv + off;
+#pragma unroll
+      for (int d = 0; d < kDT; ++d)
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4) {
+          f32x4 vk, vv;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            vk[e] = dka[d][4 * g4 + e] * a.scale;
+            vv[e] = dva[d][4 * g4 + e];
+          }
+          *(f32x4*)(dkp + 32 * d + 8 * g4 + 4 * half) = vk;
+          *(f32x4*)(dvp + 32 * d + 8 * g4 + 4 * half) = vv;
+        }
+    } else {
+      bf16* dkp = (bf16*)kr.dk + off;
+      bf16* dvp = (bf16*)kr.dv + off;
+#pragma unroll
+      for (int d = 0; d < kDT; ++d)
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4) {
+          bf16x4 vk, vv;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            vk[e] = to_bf16(dka[d][4 * g4 + e] * a.scale);
+            vv[e] = to_bf16(dva[d][4 * g4 + e]);
+          }
+          *(bf16x4*)(dkp + 32 * d + 8 * g4 + 4 * half) = vk;
+          *(bf16x4*)(dvp + 32 * d + 8 * g4 + 4 * half) = vv;
+        }
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_bwd_dkdv(const AttnArgs& a, hipStream_t s) {
+  const int n = a.total_tiles * a.kv_heads * a.batch;
+  if (n == 0) return hipSuccess;
+  // two query heads per step, at most two query ranges (the walk state stays in registers)
+  if (a.group % 2 != 0 || a.n_q > 2) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(dkdv_kernel, dim3(n), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace bdlm

@@ -68,6 +68,7 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_kernel(const AttnArgs a) {
     const float z = qr.lse[((int64_t)it.b * H + it.h) * qr.bstride + my_row];
     lse2 = (z == -INFINITY) ? INFINITY : z * kLog2e;
     dl = qr.delta[((int64_t)it.b * H + it.h) * qr.len + my_row];
+    if (a.stats_form) dl = -dl;  // the workspace holds -D
   }
 
   f32x16 acc[DT];

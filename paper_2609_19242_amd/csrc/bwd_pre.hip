@@ -1,9 +1,13 @@
 // Backward pre-pass, gfx950 (an HBM-bound elementwise pass).
 //
 // D[b][h][row] = sum_d dO * O in fp32: the row dot the softmax gradient
-// dS = P * (dP - D) needs (arXiv 2609.19242 App. C reuses the saved O), and
-// L2[b][h][row] = LSE * log2(e) (+inf for rows that see no key, so that
-// exp2(s - L2) is 0 for them), the form the dK/dV kernel stages into LDS.
+// dS = P * (dP - D) needs (arXiv 2609.19242 App. C reuses the saved O), and a
+// per-row form of LSE for the dK/dV kernel, in one of two forms:
+//  * form 0: L2 = LSE * log2(e) (+inf for rows that see no key, so that
+//    exp2(s - L2) is 0 for them) and D;
+//  * form 1: -LSE / scale (-inf for rows that see no key) and -D, the values
+//    the scheduled dK/dV kernel starts its score and dP accumulators at, so
+//    that P = exp2(scale log2(e) acc) and dS = P acc' need no subtraction.
 // One thread per 8 consecutive head_dim elements; the D/8 threads of one
 // (row, head) are adjacent lanes and reduce with cross-lane shuffles.  O and
 // dO are read once, with the non-temporal cache policy.
@@ -57,8 +61,13 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(const AttnArgs a) {
   if (!ok) return;
   if (chunk == 0) {
     const float z = qr.lse[(b * H + h) * qr.bstride + row];
-    qr.delta[(b * H + h) * qr.len + row] = s;
-    qr.l2[(b * H + h) * qr.len + row] = (z == -INFINITY) ? INFINITY : z * 1.44269504088896340736f;
+    if (a.stats_form) {
+      qr.delta[(b * H + h) * qr.len + row] = -s;
+      qr.l2[(b * H + h) * qr.len + row] = (z == -INFINITY) ? -INFINITY : -z / a.scale;
+    } else {
+      qr.delta[(b * H + h) * qr.len + row] = s;
+      qr.l2[(b * H + h) * qr.len + row] = (z == -INFINITY) ? INFINITY : z * 1.44269504088896340736f;
+    }
   }
 }
 

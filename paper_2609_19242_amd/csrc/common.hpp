@@ -150,7 +150,7 @@ struct AttnArgs {
   int32_t window;      // clean keys per query at most (0: no limit)
   int32_t nblk;        // blocks per stream, L / M
   int32_t L;
-  int32_t pad_rule;
+  int32_t stats_form;  // bwd workspace per query row: 0 = (LSE log2(e), D), 1 = (-LSE / scale, -D)
   const int* prefix;   // clean context end per corrupted block (device), or null
   float scale;        // softmax scale
   float scale_log2;   // scale * log2(e): scores are kept in the base-2 domain
@@ -193,8 +193,17 @@ hipError_t launch_fwd_f32(const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_merge(const MergeArgs& a, int head_dim, int part_dtype, int out_dtype, hipStream_t s);
 hipError_t launch_bwd_pre(const AttnArgs& a, int head_dim, int dtype, hipStream_t s);
 hipError_t launch_bwd_bf16(const AttnArgs& a, int head_dim, hipStream_t s);
+hipError_t launch_bwd_dkdv(const AttnArgs& a, hipStream_t s);
 hipError_t launch_bwd_dq_bf16(const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_bwd_f32(const AttnArgs& a, int head_dim, hipStream_t s);
+
+// The dK/dV kernel of bwd_dkdv.hip (head_dim 128, single-term dK/dV products)
+// starts its score and dP accumulators at -LSE/scale and -D, so the backward
+// workspace holds those (stats form 1); the general kernel of bwd_bf16.hip and
+// the fp32 kernel read LSE log2(e) and D (form 0).
+inline bool dkdv_uses_scheduled_kernel(int dtype_bf16, int head_dim, int hilo, int group, int n_q) {
+  return dtype_bf16 && head_dim == 128 && !(hilo & kHiloDkDv) && group % 2 == 0 && n_q <= 2;
+}
 
 // Tile heights the launchers use (the C ABI fills ntiles/tile0 with them).
 constexpr int kFwdRowsBf16 = 256;  // query rows per forward / dQ workgroup (8 waves x 32)
