@@ -95,6 +95,14 @@ typedef enum {
 #define BDLM_HILO_DKDV 2 /* backward dV += P^T dO and dK += dS^T Q */
 #define BDLM_HILO_DQ 4   /* backward dQ += dS K */
 #define BDLM_HILO_ALL 7
+/* With any of the bits above: a selected product carries the second term only where some
+   probability P of the block of operands it contracts reaches 1/64, and a single bf16 term
+   elsewhere.  The blocks are one wave's 32 query rows x 16 keys (P V, dS K) or 32 keys x 16 query
+   rows of one query head (P^T dO, dS^T Q); the forward tests P against the row's running sum,
+   which can only over-select.  An element left single-term has P < 1/64, so its rounding error is
+   below 2^-15 in P and below 2^-15 |dP - D| in dS.  Same results as the all-tiles form up to
+   rounding; fewer matrix products where large probabilities are rare. */
+#define BDLM_HILO_ADAPTIVE 8
 
 /* Limits of one call (kernel-argument capacity). */
 #define BDLM_MAX_Q_RANGES 4
@@ -116,9 +124,10 @@ typedef struct {
   int32_t hilo;       /* bf16 path: a mask of BDLM_HILO_* bits.  A product whose bit is clear takes
                          its operand P (softmax probabilities) or dS = P (dP - D) rounded to bf16;
                          a product whose bit is set takes it as a two-term bf16 sum hi + lo (about
-                         16 significant bits, twice the matrix work of that product).  For inputs
-                         with large scores or |dS|, e.g. keys of large norm.  Ignored by the fp32
-                         path. */
+                         16 significant bits, twice the matrix work of that product), on every
+                         tile or, with BDLM_HILO_ADAPTIVE, only on tiles holding a large P.  For
+                         inputs with large scores or |dS|, e.g. keys of large norm.  Ignored by
+                         the fp32 path. */
   int64_t window;     /* 0: no limit.  > 0: a query sees only the last `window` positions of its clean
                          context (sliding-window layers; see "Mask generalisations" above) */
   const int32_t* clean_prefix; /* NULL, or a device array of L / block_size ints: the end of the clean

@@ -22,7 +22,7 @@ import torch  # noqa: F401  (load torch's HIP runtime first)
 __all__ = [
     "Problem", "Range", "BdlmError", "lib", "library_path",
     "BF16", "F32", "CLEAN", "CORRUPTED", "CLEAN_INTRA_CAUSAL", "CLEAN_INTRA_BLOCK",
-    "HILO_PV", "HILO_DKDV", "HILO_DQ", "HILO_ALL",
+    "HILO_PV", "HILO_DKDV", "HILO_DQ", "HILO_ALL", "HILO_ADAPTIVE",
     "make_problem", "joint_ranges", "attn_fwd", "attn_partial_fwd", "lse_merge",
     "attn_bwd_workspace_bytes", "attn_bwd", "attn_bwd_noalloc", "visible_pairs",
     "joint_fwd", "joint_bwd", "timing_enable", "timing_collect", "useful_flops",
@@ -34,6 +34,7 @@ CLEAN_INTRA_CAUSAL, CLEAN_INTRA_BLOCK = 0, 1
 # bdlm_problem.hilo bits: products that take P or dS as two bf16 terms
 HILO_PV, HILO_DKDV, HILO_DQ = 1, 2, 4
 HILO_ALL = HILO_PV | HILO_DKDV | HILO_DQ
+HILO_ADAPTIVE = 8  # with the bits above: the second term only on tiles holding a probability >= 1/64
 MAX_Q_RANGES, MAX_K_RANGES, MAX_MERGE_PARTS = 4, 32, 32
 NOALLOC_SCRATCH_BYTES = 64 << 20  # BDLM_NOALLOC_SCRATCH_BYTES
 
@@ -161,8 +162,9 @@ def _dtype_code(dt: torch.dtype) -> int:
 def make_problem(batch: int, L: int, block_size: int, heads: int, kv_heads: int, head_dim: int,
                  dtype, scale: float = 0.0, clean_intra: int = CLEAN_INTRA_CAUSAL, out_f32: bool = False,
                  hilo=False, window: int = 0, clean_prefix: Optional[torch.Tensor] = None) -> Problem:
-    """Problem record.  ``hilo`` is a mask of ``HILO_*`` bits (``True`` means all of them): the
-    products that take P or dS as two bf16 terms.  ``window`` limits every query to the last ``window`` positions of its clean
+    """Problem record.  ``hilo`` is a mask of ``HILO_*`` bits (``True`` means the three product bits): the
+    products that take P or dS as two bf16 terms, on every tile or, with ``HILO_ADAPTIVE``, only on
+    tiles holding a large probability.  ``window`` limits every query to the last ``window`` positions of its clean
     context (0: no limit); ``clean_prefix`` is an int32 device tensor of ``L // block_size`` entries,
     the end of corrupted block b's clean context (DFlash2 anchors), kept alive by the caller until the
     kernels that use it have run."""

@@ -13,6 +13,10 @@
 
 #include "common.hpp"
 
+static_assert(BDLM_HILO_PV == bdlm::kHiloPv && BDLM_HILO_DKDV == bdlm::kHiloDkDv && BDLM_HILO_DQ == bdlm::kHiloDq &&
+                  BDLM_HILO_ADAPTIVE == bdlm::kHiloAdaptive,
+              "hilo bits of the C ABI and the kernels agree");
+
 using namespace bdlm;
 
 namespace {
@@ -93,8 +97,9 @@ bdlm_status check_problem(const bdlm_problem* p) {
     return fail(BDLM_ERR_INVALID, "clean_intra %d is not a bdlm_clean_intra value", p->clean_intra);
   if (!std::isfinite(p->scale)) return fail(BDLM_ERR_INVALID, "scale is not finite");
   if (p->out_f32 != 0 && p->out_f32 != 1) return fail(BDLM_ERR_INVALID, "out_f32 must be 0 or 1");
-  if (p->hilo < 0 || p->hilo > BDLM_HILO_ALL)
-    return fail(BDLM_ERR_INVALID, "hilo must be a mask of BDLM_HILO_* bits (0..%d, got %d)", BDLM_HILO_ALL, p->hilo);
+  if (p->hilo < 0 || p->hilo > (BDLM_HILO_ALL | BDLM_HILO_ADAPTIVE))
+    return fail(BDLM_ERR_INVALID, "hilo must be a mask of BDLM_HILO_* bits (0..%d, got %d)",
+                BDLM_HILO_ALL | BDLM_HILO_ADAPTIVE, p->hilo);
   if (p->window < 0 || p->window >= kMaxPos)
     return fail(BDLM_ERR_INVALID, "window must be in [0, 2^30) (got %lld)", (long long)p->window);
   if (p->clean_prefix && (reinterpret_cast<uintptr_t>(p->clean_prefix) & 3u) != 0)
@@ -147,6 +152,7 @@ void fill_common(AttnArgs& a, const bdlm_problem* p) {
   a.scale_log2 = a.scale * 1.44269504088896340736f;
   a.out_f32 = (p->dtype == BDLM_F32 || p->out_f32) ? 1 : 0;
   a.hilo = p->hilo;
+  a.hilo_tau = (p->hilo & BDLM_HILO_ADAPTIVE) ? kHiloTau : 0.f;
 }
 
 void fill_q(QRangeArg& d, const bdlm_range& r) {

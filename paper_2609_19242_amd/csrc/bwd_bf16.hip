@@ -56,7 +56,9 @@ struct CopyPlan {
 
 // NQ: query-range slots the walk considers (2 when the call has at most two
 // query ranges, else kMaxQ); fewer slots keep the walk state in fewer registers.
-template <int D, bool HILO, int NH, int NQ>
+// HM: 0 single-term P and dS, 1 two-term on every step, 2 two-term on the
+// 16-query halves of a step holding a probability of at least hilo_tau.
+template <int D, int HM, int NH, int NQ>
 __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
   constexpr int BN = kBwdKeysBf16, BM = 32, KS = D / 16, DT = D / 32;
   using Stage = BwdStage<D, NH>;
@@ -275,71 +277,233 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
     // Row reads: lane (half, l32) reads logical chunk 2k + half of row l32,
     // i.e. zr ^ 32k; heads and the dO tensor are immediate offsets.
     const uint32_t zr = lds_addr(&S) + yrow;
-    f32x16 sacc[NH], dpacc[NH];
+    if constexpr (HM == 0) {
+      f32x16 sacc[NH], dpacc[NH];
 #pragma unroll
-    for (int j = 0; j < NH; ++j) {
+      for (int j = 0; j < NH; ++j) {
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        sacc[j][i] = 0.f;
-        dpacc[j][i] = 0.f;
-      }
+        for (int i = 0; i < 16; ++i) {
+          sacc[j][i] = 0.f;
+          dpacc[j][i] = 0.f;
+        }
 #pragma unroll
-      for (int k = 0; k < KS; ++k) {
-        const uint32_t a = (zr ^ (32u * k)) + j * HB;
-        sacc[j] = mfma32(lds_load16(a), kf[k], sacc[j]);
-        dpacc[j] = mfma32(lds_load16(a + TB), vf[k], dpacc[j]);
-      }
-    }
-
-    // P = exp2(S c - LSE log2 e) and dS = P (dP - D) per head; the mask only
-    // on partly visible steps.  Rows past the range end read Q = dO = 0 and are
-    // always masked.
-    bf16x8 pb[NH][2], pl[NH][2], dsb[NH][2], dsl[NH][2];
-#pragma unroll
-    for (int j = 0; j < NH; ++j) {
-      if (partial) {
-#pragma unroll
-        for (int i = 0; i < 16; ++i)
-          if ((unsigned)(mbase + 8 * (i >> 2) + (i & 3)) >= (unsigned)lane_qw) sacc[j][i] = -INFINITY;
-      }
-#pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4) {
-        const f32x4 l2 = *(const f32x4*)(&S.l2[j * BM + 8 * g4 + 4 * half]);
-        const f32x4 dl = *(const f32x4*)(&S.dl[j * BM + 8 * g4 + 4 * half]);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int i = 4 * g4 + e;
-          const float p = exp2f_fast(fmaf(sacc[j][i], c, -l2[e]));
-          const float ds = p * (dpacc[j][i] - dl[e]);
-          const bf16 phi = to_bf16(p);
-          pb[j][i >> 3][i & 7] = phi;
-          if constexpr (HILO) pl[j][i >> 3][i & 7] = to_bf16(p - (float)phi);
-          const bf16 hi = to_bf16(ds);
-          dsb[j][i >> 3][i & 7] = hi;
-          if constexpr (HILO) dsl[j][i >> 3][i & 7] = to_bf16(ds - (float)hi);
+        for (int k = 0; k < KS; ++k) {
+          const uint32_t a = (zr ^ (32u * k)) + j * HB;
+          sacc[j] = mfma32(lds_load16(a), kf[k], sacc[j]);
+          dpacc[j] = mfma32(lds_load16(a + TB), vf[k], dpacc[j]);
         }
       }
-    }
 
-    // dV^T += dO^T P and dK^T += Q^T dS (queries are the contraction index),
-    // one head and one 16-query half at a time with its transposed fragments.
-    // Transpose reads: rows 16u + R0 (zt0) and 16u + R0 + 8 (zt1), logical
-    // 8-byte piece 8d + 4 (G & 1) + (sl & 3) of the row, i.e. zt ^ 64d.
-    const uint32_t zt0 = lds_addr(&S) + ytr0, zt1 = lds_addr(&S) + ytr1;
+      // P = exp2(S c - LSE log2 e) and dS = P (dP - D) per head; the mask only
+      // on partly visible steps.  Rows past the range end read Q = dO = 0 and are
+      // always masked.
+      bf16x8 pb[NH][2], dsb[NH][2];
 #pragma unroll
-    for (int j = 0; j < NH; ++j) {
+      for (int j = 0; j < NH; ++j) {
+        if (partial) {
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
+          for (int i = 0; i < 16; ++i)
+            if ((unsigned)(mbase + 8 * (i >> 2) + (i & 3)) >= (unsigned)lane_qw) sacc[j][i] = -INFINITY;
+        }
 #pragma unroll
-        for (int d = 0; d < DT; ++d) {
-          const uint32_t a0 = (zt0 ^ (64u * d)) + j * HB + u * 16 * RB;
-          const uint32_t a1 = (zt1 ^ (64u * d)) + j * HB + u * 16 * RB;
-          const bf16x8 doT = cat(lds_read_tr_at(a0 + TB), lds_read_tr_at(a1 + TB));
-          const bf16x8 qT = cat(lds_read_tr_at(a0), lds_read_tr_at(a1));
-          dva[d] = mfma32(doT, pb[j][u], dva[d]);
-          if constexpr (HILO) dva[d] = mfma32(doT, pl[j][u], dva[d]);
-          dka[d] = mfma32(qT, dsb[j][u], dka[d]);
-          if constexpr (HILO) dka[d] = mfma32(qT, dsl[j][u], dka[d]);
+        for (int g4 = 0; g4 < 4; ++g4) {
+          const f32x4 l2 = *(const f32x4*)(&S.l2[j * BM + 8 * g4 + 4 * half]);
+          const f32x4 dl = *(const f32x4*)(&S.dl[j * BM + 8 * g4 + 4 * half]);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int i = 4 * g4 + e;
+            const float p = exp2f_fast(fmaf(sacc[j][i], c, -l2[e]));
+            const float ds = p * (dpacc[j][i] - dl[e]);
+            const bf16 phi = to_bf16(p);
+            pb[j][i >> 3][i & 7] = phi;
+            const bf16 hi = to_bf16(ds);
+            dsb[j][i >> 3][i & 7] = hi;
+          }
+        }
+      }
+
+      // dV^T += dO^T P and dK^T += Q^T dS (queries are the contraction index),
+      // one head and one 16-query half at a time with its transposed fragments.
+      // Transpose reads: rows 16u + R0 (zt0) and 16u + R0 + 8 (zt1), logical
+      // 8-byte piece 8d + 4 (G & 1) + (sl & 3) of the row, i.e. zt ^ 64d.
+      const uint32_t zt0 = lds_addr(&S) + ytr0, zt1 = lds_addr(&S) + ytr1;
+#pragma unroll
+      for (int j = 0; j < NH; ++j) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+#pragma unroll
+          for (int d = 0; d < DT; ++d) {
+            const uint32_t a0 = (zt0 ^ (64u * d)) + j * HB + u * 16 * RB;
+            const uint32_t a1 = (zt1 ^ (64u * d)) + j * HB + u * 16 * RB;
+            const bf16x8 doT = cat(lds_read_tr_at(a0 + TB), lds_read_tr_at(a1 + TB));
+            const bf16x8 qT = cat(lds_read_tr_at(a0), lds_read_tr_at(a1));
+            dva[d] = mfma32(doT, pb[j][u], dva[d]);
+            dka[d] = mfma32(qT, dsb[j][u], dka[d]);
+          }
+        }
+      }
+    } else if constexpr (HM == 1) {
+      f32x16 sacc[NH], dpacc[NH];
+#pragma unroll
+      for (int j = 0; j < NH; ++j) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          sacc[j][i] = 0.f;
+          dpacc[j][i] = 0.f;
+        }
+#pragma unroll
+        for (int k = 0; k < KS; ++k) {
+          const uint32_t a = (zr ^ (32u * k)) + j * HB;
+          sacc[j] = mfma32(lds_load16(a), kf[k], sacc[j]);
+          dpacc[j] = mfma32(lds_load16(a + TB), vf[k], dpacc[j]);
+        }
+      }
+
+      // P = exp2(S c - LSE log2 e) and dS = P (dP - D) per head; the mask only
+      // on partly visible steps.  Rows past the range end read Q = dO = 0 and are
+      // always masked.
+      bf16x8 pb[NH][2], pl[NH][2], dsb[NH][2], dsl[NH][2];
+#pragma unroll
+      for (int j = 0; j < NH; ++j) {
+        if (partial) {
+#pragma unroll
+          for (int i = 0; i < 16; ++i)
+            if ((unsigned)(mbase + 8 * (i >> 2) + (i & 3)) >= (unsigned)lane_qw) sacc[j][i] = -INFINITY;
+        }
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4) {
+          const f32x4 l2 = *(const f32x4*)(&S.l2[j * BM + 8 * g4 + 4 * half]);
+          const f32x4 dl = *(const f32x4*)(&S.dl[j * BM + 8 * g4 + 4 * half]);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int i = 4 * g4 + e;
+            const float p = exp2f_fast(fmaf(sacc[j][i], c, -l2[e]));
+            const float ds = p * (dpacc[j][i] - dl[e]);
+            const bf16 phi = to_bf16(p);
+            pb[j][i >> 3][i & 7] = phi;
+            pl[j][i >> 3][i & 7] = to_bf16(p - (float)phi);
+            const bf16 hi = to_bf16(ds);
+            dsb[j][i >> 3][i & 7] = hi;
+            dsl[j][i >> 3][i & 7] = to_bf16(ds - (float)hi);
+          }
+        }
+      }
+
+      // dV^T += dO^T P and dK^T += Q^T dS (queries are the contraction index),
+      // one head and one 16-query half at a time with its transposed fragments.
+      // Transpose reads: rows 16u + R0 (zt0) and 16u + R0 + 8 (zt1), logical
+      // 8-byte piece 8d + 4 (G & 1) + (sl & 3) of the row, i.e. zt ^ 64d.
+      const uint32_t zt0 = lds_addr(&S) + ytr0, zt1 = lds_addr(&S) + ytr1;
+#pragma unroll
+      for (int j = 0; j < NH; ++j) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+#pragma unroll
+          for (int d = 0; d < DT; ++d) {
+            const uint32_t a0 = (zt0 ^ (64u * d)) + j * HB + u * 16 * RB;
+            const uint32_t a1 = (zt1 ^ (64u * d)) + j * HB + u * 16 * RB;
+            const bf16x8 doT = cat(lds_read_tr_at(a0 + TB), lds_read_tr_at(a1 + TB));
+            const bf16x8 qT = cat(lds_read_tr_at(a0), lds_read_tr_at(a1));
+            dva[d] = mfma32(doT, pb[j][u], dva[d]);
+            dva[d] = mfma32(doT, pl[j][u], dva[d]);
+            dka[d] = mfma32(qT, dsb[j][u], dka[d]);
+            dka[d] = mfma32(qT, dsl[j][u], dka[d]);
+          }
+        }
+      }
+    } else {
+      // S = Q K^T and dP = dO V^T of head j of the pair.
+      auto scores = [&](int j, f32x16& sa, f32x16& dpa) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          sa[i] = 0.f;
+          dpa[i] = 0.f;
+        }
+#pragma unroll
+        for (int k = 0; k < KS; ++k) {
+          const uint32_t a = (zr ^ (32u * k)) + j * HB;
+          sa = mfma32(lds_load16(a), kf[k], sa);
+          dpa = mfma32(lds_load16(a + TB), vf[k], dpa);
+        }
+      };
+      // P = exp2(S c - LSE log2 e) and dS = P (dP - D) of head j, to bf16 (with
+      // lo, the rounding residuals); the mask only on partly visible steps.
+      // Rows past the range end read Q = dO = 0 and are always masked.
+      auto probs = [&](int j, f32x16& sa, const f32x16& dpa, bf16x8 (&pp)[2], bf16x8 (&dd)[2], float (&pmax)[2],
+                       auto lo) __attribute__((always_inline)) {
+        if (partial) {
+#pragma unroll
+          for (int i = 0; i < 16; ++i)
+            if ((unsigned)(mbase + 8 * (i >> 2) + (i & 3)) >= (unsigned)lane_qw) sa[i] = -INFINITY;
+        }
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4) {
+          const f32x4 l2 = *(const f32x4*)(&S.l2[j * BM + 8 * g4 + 4 * half]);
+          const f32x4 dl = *(const f32x4*)(&S.dl[j * BM + 8 * g4 + 4 * half]);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const int i = 4 * g4 + e;
+            const float p = exp2f_fast(fmaf(sa[i], c, -l2[e]));
+            const float ds = p * (dpa[i] - dl[e]);
+            if constexpr (decltype(lo)::value) {
+              pp[i >> 3][i & 7] = to_bf16(p - (float)to_bf16(p));
+              dd[i >> 3][i & 7] = to_bf16(ds - (float)to_bf16(ds));
+            } else {
+              pp[i >> 3][i & 7] = to_bf16(p);
+              dd[i >> 3][i & 7] = to_bf16(ds);
+              pmax[i >> 3] = fmaxf(pmax[i >> 3], p);
+            }
+          }
+        }
+      };
+
+      // dV^T += dO^T P and dK^T += Q^T dS (queries are the contraction index),
+      // one head and one 16-query half at a time with its transposed fragments.
+      // Transpose reads: rows 16u + R0 (zt0) and 16u + R0 + 8 (zt1), logical
+      // 8-byte piece 8d + 4 (G & 1) + (sl & 3) of the row, i.e. zt ^ 64d.
+      const uint32_t zt0 = lds_addr(&S) + ytr0, zt1 = lds_addr(&S) + ytr1;
+      auto products = [&](int j, const bf16x8 (&pp)[2], const bf16x8 (&dd)[2]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+#pragma unroll
+          for (int d = 0; d < DT; ++d) {
+            const uint32_t a0 = (zt0 ^ (64u * d)) + j * HB + u * 16 * RB;
+            const uint32_t a1 = (zt1 ^ (64u * d)) + j * HB + u * 16 * RB;
+            const bf16x8 doT = cat(lds_read_tr_at(a0 + TB), lds_read_tr_at(a1 + TB));
+            const bf16x8 qT = cat(lds_read_tr_at(a0), lds_read_tr_at(a1));
+            dva[d] = mfma32(doT, pp[u], dva[d]);
+            dka[d] = mfma32(qT, dd[u], dka[d]);
+          }
+        }
+      };
+      // Two-term products, one head at a time: a 16-query half of the head
+      // also carries P - bf16(P) and dS - bf16(dS) as second bf16 terms when
+      // some probability in it reaches hilo_tau.
+#pragma unroll
+      for (int j = 0; j < NH; ++j) {
+        f32x16 sa, dpa;
+        scores(j, sa, dpa);
+        bf16x8 pb[2], dsb[2];
+        float pmax[2] = {0.f, 0.f};
+        probs(j, sa, dpa, pb, dsb, pmax, std::false_type{});
+        products(j, pb, dsb);
+        const bool two0 = __builtin_amdgcn_ballot_w64(pmax[0] >= a.hilo_tau) != 0;
+        const bool two1 = __builtin_amdgcn_ballot_w64(pmax[1] >= a.hilo_tau) != 0;
+        if (two0 || two1) {
+          bf16x8 pl[2], dsl[2];
+          probs(j, sa, dpa, pl, dsl, pmax, std::true_type{});
+#pragma unroll
+          for (int u = 0; u < 2; ++u) {
+            if (u == 0 ? two0 : two1) {
+#pragma unroll
+              for (int d = 0; d < DT; ++d) {
+                const uint32_t a0 = (zt0 ^ (64u * d)) + j * HB + u * 16 * RB;
+                const uint32_t a1 = (zt1 ^ (64u * d)) + j * HB + u * 16 * RB;
+                dva[d] = mfma32(cat(lds_read_tr_at(a0 + TB), lds_read_tr_at(a1 + TB)), pl[u], dva[d]);
+                dka[d] = mfma32(cat(lds_read_tr_at(a0), lds_read_tr_at(a1)), dsl[u], dka[d]);
+              }
+            }
+          }
         }
       }
     }
@@ -414,30 +578,32 @@ __global__ __launch_bounds__(256) void bwd_bf16_kernel(const AttnArgs a) {
 
 }  // namespace
 
-template <int D, bool HILO, int NQ>
+template <int D, int HM, int NQ>
 void launch_nh(const AttnArgs& a, int n, hipStream_t s) {
   if (a.group % 2 == 0)
-    hipLaunchKernelGGL((bwd_bf16_kernel<D, HILO, 2, NQ>), dim3(n), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((bwd_bf16_kernel<D, HM, 2, NQ>), dim3(n), dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL((bwd_bf16_kernel<D, HILO, 1, NQ>), dim3(n), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((bwd_bf16_kernel<D, HM, 1, NQ>), dim3(n), dim3(256), 0, s, a);
 }
 
-template <int D, bool HILO>
+template <int D, int HM>
 void launch_nq(const AttnArgs& a, int n, hipStream_t s) {
-  if (a.n_q <= 2) launch_nh<D, HILO, 2>(a, n, s);
-  else launch_nh<D, HILO, kMaxQ>(a, n, s);
+  if (a.n_q <= 2) launch_nh<D, HM, 2>(a, n, s);
+  else launch_nh<D, HM, kMaxQ>(a, n, s);
+}
+
+template <int D>
+void launch_hm(const AttnArgs& a, int n, hipStream_t s) {
+  if (!(a.hilo & kHiloDkDv)) launch_nq<D, 0>(a, n, s);
+  else if (!(a.hilo & kHiloAdaptive)) launch_nq<D, 1>(a, n, s);
+  else launch_nq<D, 2>(a, n, s);
 }
 
 hipError_t launch_bwd_bf16(const AttnArgs& a, int head_dim, hipStream_t s) {
   const int n = a.total_tiles * a.kv_heads * a.batch;
   if (n == 0) return hipSuccess;
-  if (head_dim == 128) {
-    if (a.hilo & kHiloDkDv) launch_nq<128, true>(a, n, s);
-    else launch_nq<128, false>(a, n, s);
-  } else {
-    if (a.hilo & kHiloDkDv) launch_nq<64, true>(a, n, s);
-    else launch_nq<64, false>(a, n, s);
-  }
+  if (head_dim == 128) launch_hm<128>(a, n, s);
+  else launch_hm<64>(a, n, s);
   return hipGetLastError();
 }
 

@@ -70,6 +70,11 @@ constexpr int kIPW = 8;
 __device__ __forceinline__ void mfma_agpr(f32x16& acc, const bf16x8& a, const bf16x8& b) {
   asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
 }
+// The same with the two wait states a VALU write of an operand needs before an
+// MFMA reads it (the compiler does not pad inline assembly for it).
+__device__ __forceinline__ void mfma_agpr_padded(f32x16& acc, const bf16x8& a, const bf16x8& b) {
+  asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
 
 // Buffer resource as four SGPRs for the inline-assembly copies.
 __device__ __forceinline__ u32x4 rsrc_words(const void* base, uint32_t bytes) {
@@ -98,6 +103,11 @@ __device__ __forceinline__ f32x4 lds_f4(uint32_t a) {
   return *(__attribute__((address_space(3))) const f32x4*)(uintptr_t)a;
 }
 
+// ADAPT: a step also carries P - bf16(P) and dS - bf16(dS) of a head's
+// 16-row half as second bf16 terms when some probability of that half reaches
+// hilo_tau (8 more products: head 0's after block B, head 1's inside block D,
+// each while its P and dS are still in registers).
+template <bool ADAPT>
 __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
   constexpr int BN = kBwdKeysBf16, BM = kBM, NH = kNH;
   static_assert(BN == 128, "tile shape");
@@ -364,6 +374,43 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
     }
   };
 
+  // The starts of head j of step `cu` (stage st) into s, d, with the mask of
+  // partly visible steps (the values load_starts gives that head).
+  auto load_head_starts = [&](int st, const Cursor cu, int j, f32x16& s, f32x16& d) __attribute__((always_inline)) {
+    const uint32_t base = ystat + st * kStatB;
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4) {
+      const f32x4 l = lds_f4(base + (j * BM + 8 * g4) * 4);
+      const f32x4 dd = lds_f4(base + 256 + (j * BM + 8 * g4) * 4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        s[4 * g4 + e] = l[e];
+        d[4 * g4 + e] = dd[e];
+      }
+    }
+    const int q = cu.s >= 0 ? cu.q : 0;
+    const int partial =
+        __builtin_amdgcn_readfirstlane((cu.s >= BDLM_PICK(f0, q) && cu.s < BDLM_PICK(f1, q)) ? 0 : 1);
+    if (partial) {
+      const int mbase = BDLM_PICK(pos0, q) + cu.s * BM + 4 * half - BDLM_PICK(qa, q);
+      const int lane_qw = BDLM_PICK(qw, q);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        float x0 = s[i];
+        uint32_t tmp;
+        asm volatile(
+            "v_add_u32 %1, %2, %3\n\t"
+            "v_cmp_lt_u32 vcc, %1, %4\n\t"
+            "v_mov_b32 %1, 0xff800000\n\t"
+            "v_cndmask_b32 %0, %1, %0, vcc"
+            : "+v"(x0), "=&v"(tmp)
+            : "n"(8 * (i >> 2) + (i & 3)), "v"(mbase), "v"(lane_qw)
+            : "vcc");
+        s[i] = x0;
+      }
+    }
+  };
+
   // One step on stage ST: the copies of step `cp` into stage CP go out under
   // its first products, the starts of step `nx` (stage NX) are loaded under its
   // last ones, and the walk advances under the softmax of head 0.
@@ -386,6 +433,7 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
     }
     fence();
     bf16x8 pb[NH][2], dsb[NH][2];
+    float pm[NH][2] = {{0.f, 0.f}, {0.f, 0.f}};  // ADAPT: largest P per head and 16-row half
     Cursor c4;
 #pragma unroll
     for (int n = 0; n < 2 * kKS; ++n) {
@@ -413,6 +461,7 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
           const float p = exp2f_fast(sa[0][i] * c);
           da[0][i] = p * da[0][i];
           sa[0][i] = p;
+          if constexpr (ADAPT) pm[0][i >> 3] = fmaxf(pm[0][i >> 3], p);
         }
         if (k & 1) {
           const int i0 = 2 * (k - 1);
@@ -438,6 +487,32 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
     };
     // product m of a head: m < 8 -> dV (u = m / 4, d = m % 4), else dK
     auto opnd = [&](int j, int m) { return m < 8 ? trd(j, m / 4, m % 4) : trq(j, (m - 8) / 4, (m - 8) % 4); };
+    // ADAPT: the 16-row half u of head j also carries P - bf16(P) and
+    // dS - bf16(dS) (from P_j and dS_j, still in sa[j], da[j]) as second bf16
+    // terms when some probability of that half reaches hilo_tau: 4 dV and 4 dK
+    // products more.
+    auto second_terms = [&](int j) __attribute__((always_inline)) {
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        if (__builtin_amdgcn_ballot_w64(pm[j][u] >= a.hilo_tau) != 0) {
+          bf16x8 pl, dl;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float p = sa[j][8 * u + e], ds = da[j][8 * u + e];
+            pl[e] = to_bf16(p - (float)to_bf16(p));
+            dl[e] = to_bf16(ds - (float)to_bf16(ds));
+          }
+#pragma unroll
+          for (int d = 0; d < kDT; ++d) mfma_agpr_padded(dva[d], trd(j, u, d), pl);
+#pragma unroll
+          for (int d = 0; d < kDT; ++d) mfma_agpr_padded(dka[d], trq(j, u, d), dl);
+        }
+      }
+    };
+    if constexpr (ADAPT) {
+      second_terms(0);
+      fence();
+    }
     bf16x8 tf[TA + 1];
 #pragma unroll
     for (int n = 0; n < TA; ++n) tf[n] = opnd(0, n);
@@ -451,6 +526,7 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
       if (j == 0) {
         // P_1 = exp2(c S_1): one score per product
         sa[1][m] = exp2f_fast(sa[1][m] * c);
+        if constexpr (ADAPT) pm[1][m >> 3] = fmaxf(pm[1][m >> 3], sa[1][m]);
         if (m & 1) {
           pb[1][m >> 3][(m - 1) & 7] = to_bf16(sa[1][m - 1]);
           pb[1][m >> 3][m & 7] = to_bf16(sa[1][m]);
@@ -468,8 +544,16 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
           for (int e = 0; e < 4; ++e) dsb[1][(i0 + e) >> 3][(i0 + e) & 7] = to_bf16(da[1][i0 + e]);
         }
       } else if (m == 8) {
-        load_starts(NX, c1);
+        if constexpr (!ADAPT) load_starts(NX, c1);
+        else load_head_starts(NX, c1, 0, sa[0], da[0]);
       }
+      fence();
+    }
+    if constexpr (ADAPT) {
+      // head 1's second terms need P_1 and dS_1, which its next starts
+      // overwrite: both come after the products here
+      second_terms(1);
+      load_head_starts(NX, c1, 1, sa[1], da[1]);
       fence();
     }
     asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(kIPW + 1) : "memory");
@@ -562,7 +646,9 @@ hipError_t launch_bwd_dkdv(const AttnArgs& a, hipStream_t s) {
   if (n == 0) return hipSuccess;
   // two query heads per step, at most two query ranges (the walk state stays in registers)
   if (a.group % 2 != 0 || a.n_q > 2) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(dkdv_kernel, dim3(n), dim3(256), 0, s, a);
+  if (!(a.hilo & kHiloDkDv)) hipLaunchKernelGGL(dkdv_kernel<false>, dim3(n), dim3(256), 0, s, a);
+  else if (a.hilo & kHiloAdaptive) hipLaunchKernelGGL(dkdv_kernel<true>, dim3(n), dim3(256), 0, s, a);
+  else return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

@@ -19,7 +19,7 @@ namespace {
 
 constexpr float kLog2e = 1.44269504088896340736f;
 
-template <int D, int NW, bool HILO>
+template <int D, int NW, int HM>
 __global__ __launch_bounds__(NW * 64) void bwd_dq_kernel(const AttnArgs a) {
   constexpr int BM = NW * 32, BN = 64, KS = D / 16, DT = D / 32;
   // K and V tiles with swizzled rows: K serves both its row reads (S^T) and
@@ -207,9 +207,11 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_kernel(const AttnArgs a) {
         }
     }
 
-    // dS^T = P^T (dP^T - D) in the S^T register layout, rounded to bf16
-    // (with HILO also the rounding residual, a second bf16 term).
+    // dS^T = P^T (dP^T - D) in the S^T register layout, rounded to bf16; HM 1
+    // adds dS - bf16(dS) as a second bf16 term on every tile, HM 2 on the
+    // 16-key chunks that hold a probability of at least hilo_tau.
     bf16x8 dsb[4], dsl[4];
+    float cmax[4] = {0.f, 0.f, 0.f, 0.f};  // HM 2: largest P per 16-key chunk
 #pragma unroll
     for (int u = 0; u < 2; ++u)
 #pragma unroll
@@ -218,19 +220,50 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_kernel(const AttnArgs a) {
         const float ds = p * (dpacc[u][i] - dl);
         const bf16 hi = to_bf16(ds);
         dsb[u * 2 + (i >> 3)][i & 7] = hi;
-        if constexpr (HILO) dsl[u * 2 + (i >> 3)][i & 7] = to_bf16(ds - (float)hi);
+        if constexpr (HM != 0) dsl[u * 2 + (i >> 3)][i & 7] = to_bf16(ds - (float)hi);
+        if constexpr (HM == 2) cmax[u * 2 + (i >> 3)] = fmaxf(cmax[u * 2 + (i >> 3)], p);
       }
 
     // dQ^T[d][q] += sum_key K[key][d] dS[q][key]; key order per 16-key step as in the forward.
     const uint32_t zt0 = sb + ytr0, zt1 = sb + ytr1;  // K tile by transpose reads
+    auto dsk = [&](const bf16x8 (&dd)[4]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+      for (int u = 0; u < 4; ++u) {
 #pragma unroll
-      for (int d = 0; d < DT; ++d) {
-        const bf16x8 ka = cat(lds_read_tr_at((zt0 ^ (64u * d)) + u * 16 * RB),
-                              lds_read_tr_at((zt1 ^ (64u * d)) + u * 16 * RB));
-        acc[d] = mfma32(ka, dsb[u], acc[d]);
-        if constexpr (HILO) acc[d] = mfma32(ka, dsl[u], acc[d]);
+        for (int d = 0; d < DT; ++d) {
+          const bf16x8 ka = cat(lds_read_tr_at((zt0 ^ (64u * d)) + u * 16 * RB),
+                                lds_read_tr_at((zt1 ^ (64u * d)) + u * 16 * RB));
+          acc[d] = mfma32(ka, dd[u], acc[d]);
+        }
+      }
+    };
+    if constexpr (HM == 1) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+#pragma unroll
+        for (int d = 0; d < DT; ++d) {
+          const bf16x8 ka = cat(lds_read_tr_at((zt0 ^ (64u * d)) + u * 16 * RB),
+                                lds_read_tr_at((zt1 ^ (64u * d)) + u * 16 * RB));
+          acc[d] = mfma32(ka, dsb[u], acc[d]);
+          acc[d] = mfma32(ka, dsl[u], acc[d]);
+        }
+      }
+    } else {
+      dsk(dsb);
+      if constexpr (HM == 2) {
+        // second terms of the 16-key chunks holding a probability >= hilo_tau
+        // (K^T fragments re-read)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          if (__builtin_amdgcn_ballot_w64(cmax[u] >= a.hilo_tau) != 0) {
+#pragma unroll
+            for (int d = 0; d < DT; ++d) {
+              const bf16x8 ka = cat(lds_read_tr_at((zt0 ^ (64u * d)) + u * 16 * RB),
+                                    lds_read_tr_at((zt1 ^ (64u * d)) + u * 16 * RB));
+              acc[d] = mfma32(ka, dsl[u], acc[d]);
+            }
+          }
+        }
       }
     }
 
@@ -271,20 +304,25 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_kernel(const AttnArgs a) {
   }
 }
 
+// HM of the kernel: 0 single-term P (dS), 1 two-term on every tile, 2
+// two-term on the 16-key chunks holding a large probability.
+template <int D>
+void launch_hm(const AttnArgs& a, int n, hipStream_t s) {
+  constexpr int NW = kFwdRowsBf16 / 32;
+  const int hm = !(a.hilo & kHiloDq) ? 0 : (a.hilo & kHiloAdaptive) ? 2 : 1;
+  if (hm == 0) hipLaunchKernelGGL((bwd_dq_kernel<D, NW, 0>), dim3(n), dim3(NW * 64), 0, s, a);
+  else if (hm == 1) hipLaunchKernelGGL((bwd_dq_kernel<D, NW, 1>), dim3(n), dim3(NW * 64), 0, s, a);
+  else hipLaunchKernelGGL((bwd_dq_kernel<D, NW, 2>), dim3(n), dim3(NW * 64), 0, s, a);
+}
+
 }  // namespace
 
 // a.total_tiles / qr[i].tile0 / ntiles must describe kFwdRowsBf16-row query tiles.
 hipError_t launch_bwd_dq_bf16(const AttnArgs& a, int head_dim, hipStream_t s) {
-  constexpr int NW = kFwdRowsBf16 / 32;
   const int n = a.total_tiles * a.heads * a.batch;
   if (n == 0) return hipSuccess;
-  if (head_dim == 128) {
-    if (a.hilo & kHiloDq) hipLaunchKernelGGL((bwd_dq_kernel<128, NW, true>), dim3(n), dim3(NW * 64), 0, s, a);
-    else hipLaunchKernelGGL((bwd_dq_kernel<128, NW, false>), dim3(n), dim3(NW * 64), 0, s, a);
-  } else {
-    if (a.hilo & kHiloDq) hipLaunchKernelGGL((bwd_dq_kernel<64, NW, true>), dim3(n), dim3(NW * 64), 0, s, a);
-    else hipLaunchKernelGGL((bwd_dq_kernel<64, NW, false>), dim3(n), dim3(NW * 64), 0, s, a);
-  }
+  if (head_dim == 128) launch_hm<128>(a, n, s);
+  else launch_hm<64>(a, n, s);
   return hipGetLastError();
 }
 

@@ -26,6 +26,8 @@ constexpr int kMaxQ = 4;
 constexpr int kHiloPv = 1;    // forward P V
 constexpr int kHiloDkDv = 2;  // backward P^T dO and dS^T Q (dK/dV kernel)
 constexpr int kHiloDq = 4;    // backward dS K (dQ kernel)
+constexpr int kHiloAdaptive = 8;  // the second term only on tiles where some probability reaches kHiloTau
+constexpr float kHiloTau = 1.0f / 64;
 constexpr int kMaxK = 32;
 constexpr int kMaxParts = 32;
 constexpr int kBig = 0x3fffffff;  // "to the end of the stream" (positions stay below 2^30)
@@ -158,6 +160,7 @@ struct AttnArgs {
   int32_t interleave;    // fwd: query ranges have equal tile counts, visit them round-robin
   int32_t out_f32;       // O, dQ, dK, dV are fp32 (else the input dtype)
   int32_t hilo;          // kHilo* bits: products whose P or dS operand is bf16 hi + lo
+  float hilo_tau;        // those products take the second term only on tiles where some P reaches this (0: all tiles)
   int32_t order[kMaxK];  // bwd: visiting order of key ranges (heaviest first)
   QRangeArg qr[kMaxQ];
   KRangeArg kr[kMaxK];
@@ -197,12 +200,14 @@ hipError_t launch_bwd_dkdv(const AttnArgs& a, hipStream_t s);
 hipError_t launch_bwd_dq_bf16(const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_bwd_f32(const AttnArgs& a, int head_dim, hipStream_t s);
 
-// The dK/dV kernel of bwd_dkdv.hip (head_dim 128, single-term dK/dV products)
-// starts its score and dP accumulators at -LSE/scale and -D, so the backward
+// The dK/dV kernel of bwd_dkdv.hip (head_dim 128, single-term or adaptive
+// two-term dK/dV products, an even GQA group, at most two query ranges with
+// rows) starts its score and dP accumulators at -LSE/scale and -D, so the backward
 // workspace holds those (stats form 1); the general kernel of bwd_bf16.hip and
 // the fp32 kernel read LSE log2(e) and D (form 0).
 inline bool dkdv_uses_scheduled_kernel(int dtype_bf16, int head_dim, int hilo, int group, int n_q) {
-  return dtype_bf16 && head_dim == 128 && !(hilo & kHiloDkDv) && group % 2 == 0 && n_q <= 2;
+  const bool terms_ok = !(hilo & kHiloDkDv) || (hilo & kHiloAdaptive);
+  return dtype_bf16 && head_dim == 128 && terms_ok && group % 2 == 0 && n_q <= 2;
 }
 
 // Tile heights the launchers use (the C ABI fills ntiles/tile0 with them).

@@ -29,7 +29,7 @@ namespace {
 constexpr float kLn2 = 0.69314718055994530942f;
 constexpr float kSlack = 8.f;  // largest exponent p = exp2(s c - m_run) may reach before m_run moves
 
-template <int D, int NW, bool HILO>
+template <int D, int NW, int HM>
 __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
   constexpr int BM = NW * 32, BN = 64, KS = D / 16, DT = D / 32;
   constexpr uint32_t RB = D * 2, TB = BN * RB;  // row and tile bytes in LDS
@@ -223,7 +223,12 @@ __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
     }
     const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
     float psum = 0.f;
+    // HM 2: a 16-key chunk of the tile also carries P - bf16(P) as a second
+    // bf16 term when some lane's largest p in it reaches hilo_tau times the
+    // lane's running sum.  The row sum only grows, so an element whose final
+    // probability reaches hilo_tau always passes this test.
     bf16x8 pb[4], pl[4];
+    float cmax[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int u = 0; u < 2; ++u)
 #pragma unroll
@@ -232,21 +237,52 @@ __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
         psum += p;
         const bf16 hi = to_bf16(p);
         pb[u * 2 + (i >> 3)][i & 7] = hi;
-        if constexpr (HILO) pl[u * 2 + (i >> 3)][i & 7] = to_bf16(p - (float)hi);
+        if constexpr (HM != 0) pl[u * 2 + (i >> 3)][i & 7] = to_bf16(p - (float)hi);
+        if constexpr (HM == 2) cmax[u * 2 + (i >> 3)] = fmaxf(cmax[u * 2 + (i >> 3)], p);
       }
+    const float lim = a.hilo_tau * l_run;
     l_run += psum;
 
     // O^T[d][q] += sum_key V[key][d] P[q][key]; the key order inside each
     // 16-key step follows the S^T register layout (see device.hpp).
     const uint32_t zt0 = sb + TB + ytr0, zt1 = sb + TB + ytr1;  // V tile by transpose reads
+    auto pv = [&](const bf16x8 (&pp)[4]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+      for (int u = 0; u < 4; ++u) {
 #pragma unroll
-      for (int d = 0; d < DT; ++d) {
-        const bf16x8 va = cat(lds_read_tr_at((zt0 ^ (64u * d)) + u * 16 * RB),
-                              lds_read_tr_at((zt1 ^ (64u * d)) + u * 16 * RB));
-        acc[d] = mfma32(va, pb[u], acc[d]);
-        if constexpr (HILO) acc[d] = mfma32(va, pl[u], acc[d]);
+        for (int d = 0; d < DT; ++d) {
+          const bf16x8 va = cat(lds_read_tr_at((zt0 ^ (64u * d)) + u * 16 * RB),
+                                lds_read_tr_at((zt1 ^ (64u * d)) + u * 16 * RB));
+          acc[d] = mfma32(va, pp[u], acc[d]);
+        }
+      }
+    };
+    if constexpr (HM == 1) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+#pragma unroll
+        for (int d = 0; d < DT; ++d) {
+          const bf16x8 va = cat(lds_read_tr_at((zt0 ^ (64u * d)) + u * 16 * RB),
+                                lds_read_tr_at((zt1 ^ (64u * d)) + u * 16 * RB));
+          acc[d] = mfma32(va, pb[u], acc[d]);
+          acc[d] = mfma32(va, pl[u], acc[d]);
+        }
+      }
+    } else {
+      pv(pb);
+      if constexpr (HM == 2) {
+        // second terms of the chunks that hold a large p (V^T fragments re-read)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          if (__builtin_amdgcn_ballot_w64(cmax[u] >= lim) != 0) {
+#pragma unroll
+            for (int d = 0; d < DT; ++d) {
+              const bf16x8 va = cat(lds_read_tr_at((zt0 ^ (64u * d)) + u * 16 * RB),
+                                    lds_read_tr_at((zt1 ^ (64u * d)) + u * 16 * RB));
+              acc[d] = mfma32(va, pl[u], acc[d]);
+            }
+          }
+        }
       }
     }
 
@@ -294,19 +330,24 @@ __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
   }
 }
 
+// HM of the kernel: 0 single-term P (dS), 1 two-term on every tile, 2
+// two-term on the 16-key chunks holding a large probability.
+template <int D>
+void launch_hm(const AttnArgs& a, int n, hipStream_t s) {
+  constexpr int NW = kFwdRowsBf16 / 32;
+  const int hm = !(a.hilo & kHiloPv) ? 0 : (a.hilo & kHiloAdaptive) ? 2 : 1;
+  if (hm == 0) hipLaunchKernelGGL((fwd_bf16_kernel<D, NW, 0>), dim3(n), dim3(NW * 64), 0, s, a);
+  else if (hm == 1) hipLaunchKernelGGL((fwd_bf16_kernel<D, NW, 1>), dim3(n), dim3(NW * 64), 0, s, a);
+  else hipLaunchKernelGGL((fwd_bf16_kernel<D, NW, 2>), dim3(n), dim3(NW * 64), 0, s, a);
+}
+
 }  // namespace
 
 hipError_t launch_fwd_bf16(const AttnArgs& a, int head_dim, hipStream_t s) {
-  constexpr int NW = kFwdRowsBf16 / 32;
   const int n = a.total_tiles * a.heads * a.batch;
   if (n == 0) return hipSuccess;
-  if (head_dim == 128) {
-    if (a.hilo & kHiloPv) hipLaunchKernelGGL((fwd_bf16_kernel<128, NW, true>), dim3(n), dim3(NW * 64), 0, s, a);
-    else hipLaunchKernelGGL((fwd_bf16_kernel<128, NW, false>), dim3(n), dim3(NW * 64), 0, s, a);
-  } else {
-    if (a.hilo & kHiloPv) hipLaunchKernelGGL((fwd_bf16_kernel<64, NW, true>), dim3(n), dim3(NW * 64), 0, s, a);
-    else hipLaunchKernelGGL((fwd_bf16_kernel<64, NW, false>), dim3(n), dim3(NW * 64), 0, s, a);
-  }
+  if (head_dim == 128) launch_hm<128>(a, n, s);
+  else launch_hm<64>(a, n, s);
   return hipGetLastError();
 }
 

@@ -66,7 +66,7 @@ def _fwd(p, qr=None, kr=None, ptr=FAKE):
     (dict(dtype=7), -2, "dtype"),
     (dict(batch=0), -1, "batch"),
     (dict(clean_intra=5), -1, "clean_intra"),
-    (dict(hilo=8), -1, "hilo"),
+    (dict(hilo=16), -1, "hilo"),
     (dict(hilo=-1), -1, "hilo"),
 ])
 @host_only

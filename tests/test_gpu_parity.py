@@ -68,7 +68,10 @@ SMALL = [
 ]
 
 
-@pytest.mark.parametrize("mode", ["bf16", "bf16-out-bf16", "bf16-hilo", "fp32"])
+HILO_OF_MODE = {"bf16-hilo": bd.HILO_ALL, "bf16-hilo-adaptive": bd.HILO_ALL | bd.HILO_ADAPTIVE}
+
+
+@pytest.mark.parametrize("mode", ["bf16", "bf16-out-bf16", "bf16-hilo", "bf16-hilo-adaptive", "fp32"])
 @pytest.mark.parametrize("reading", [0, 1], ids=["causal", "block"])
 @pytest.mark.parametrize("shape", SMALL, ids=lambda s: "L{}-M{}-H{}x{}-d{}-b{}".format(*s))
 def test_joint_small(shape, reading, mode):
@@ -76,7 +79,29 @@ def test_joint_small(shape, reading, mode):
     dtype = torch.float32 if mode == "fp32" else torch.bfloat16
     q, k, v, do = joint_inputs(L, Hq, Hkv, D, dtype, batch=B, seed=L + M + D)
     check_joint(q, k, v, do, M, reading, dtype, tag=f"L{L} M{M} r{reading}", out_f32=(mode != "bf16-out-bf16"),
-                hilo=(mode == "bf16-hilo"))
+                hilo=HILO_OF_MODE.get(mode, 0))
+
+
+@pytest.mark.parametrize("reading", [0, 1], ids=["causal", "block"])
+@pytest.mark.parametrize("hilo", ["all", "adaptive"])
+@pytest.mark.parametrize("Hq", [8, 6], ids=["group4", "group3"])
+def test_two_terms_amplified_keys(reading, hilo, Hq):
+    """Keys of large norm (3% of the key rows x8, so many rows put nearly all of their
+    probability on one key) with two-term products on every tile and on the adaptive
+    selection: batch 1, L = 2048 + 2048, block 128, Hq/2 heads, d 128, every row and
+    key against the oracle with fp32 outputs.  Both branches of the adaptive test run:
+    tiles with a large probability and tiles without one; an even GQA group takes the
+    scheduled dK/dV kernel, an odd one the general kernel."""
+    import synth
+    L, M, Hkv, D = 2048, 128, 2, 128
+    q = synth.normal((1, 2 * L, Hq, D), 9100, torch.bfloat16)
+    k32 = synth.normal((1, 2 * L, Hkv, D), 9101, torch.float32)
+    k32[:, synth.amplified_rows(2 * L, 0.03, 9104)] *= 8.0
+    k = k32.to(torch.bfloat16)
+    v = synth.normal((1, 2 * L, Hkv, D), 9102, torch.bfloat16)
+    do = synth.normal((1, 2 * L, Hq, D), 9103, torch.bfloat16)
+    h = bd.HILO_ALL | (bd.HILO_ADAPTIVE if hilo == "adaptive" else 0)
+    check_joint(q, k, v, do, M, reading, torch.bfloat16, tag=f"amplified {hilo} H{Hq} r{reading}", hilo=h)
 
 
 @pytest.mark.parametrize("reading", [0, 1], ids=["causal", "block"])

@@ -53,13 +53,14 @@ def dv_identity(dv, do, group, tag):
     assert err < 5e-3, err
 
 
-def joint_check(w, reading=0, n_random=24, hilo=False, window=0, outs=("f32",)):
+def joint_check(w, reading=0, n_random=24, hilo=False, window=0, outs=("f32",), hilos=None):
     """The workload's fused fwd+bwd against the oracle on sampled rows and enumerable key sets.
 
     ``outs``: output modes to run, each against the same oracle values: "f32"
     (the fp32 accumulators, strict tolerance) and "bf16" (outputs rounded to
     bf16 as bench.py times them: the backward then reads the rounded O, and the
-    bound adds the output rounding).
+    bound adds the output rounding).  ``hilos``: the two-term settings to run in
+    each output mode (default: ``hilo`` alone).
     """
     L, M = w.L, w.block_size
     torch.cuda.empty_cache()
@@ -96,13 +97,13 @@ def joint_check(w, reading=0, n_random=24, hilo=False, window=0, outs=("f32",)):
                                chunk=128, window=window)
         key_refs.append((name, krows, dK[:, krows], dV[:, krows]))
 
-    for mode in outs:
+    for mode, hl in [(m, h) for m in outs for h in (hilos or (hilo,))]:
         f32 = mode == "f32"
-        o, lse = bd.joint_fwd(q, k, v, M, clean_intra=reading, out_f32=f32, hilo=hilo, window=window)
-        dq, dk, dv = bd.joint_bwd(q, k, v, o, lse, do, M, clean_intra=reading, out_f32=f32, hilo=hilo,
+        o, lse = bd.joint_fwd(q, k, v, M, clean_intra=reading, out_f32=f32, hilo=hl, window=window)
+        dq, dk, dv = bd.joint_bwd(q, k, v, o, lse, do, M, clean_intra=reading, out_f32=f32, hilo=hl,
                                   window=window)
         torch.cuda.synchronize()
-        t = f"{tag} [{mode} out]"
+        t = f"{tag} [{mode} out{'' if not hilos else f', hilo {int(hl)}'}]"
         assert torch.isfinite(o).all() and torch.isfinite(lse).all()
         assert torch.isfinite(dq).all() and torch.isfinite(dk).all() and torch.isfinite(dv).all()
         dv_identity(dv, do, w.heads // w.kv_heads, t)
@@ -207,19 +208,23 @@ def test_workload_drafter32k():
     torch.cuda.empty_cache()
 
 
+HILO_128K = bd.HILO_ALL | bd.HILO_ADAPTIVE
+
+
 def test_workload_128k():
     """128K with 1% of the keys scaled x8 (logits up to about +-40), in the arithmetic
-    that meets the bar there: fp32 outputs and every P and dS product in two bf16
-    terms.  Single terms fail in each kernel: P V and dS K leave about 7e-2 in dQ
-    (|dS| up to about 30, and D = rowsum(dO O) inherits O's P rounding), P^T dO
-    leaves 5.4e-2 in dV of a corrupted block whose queries put P near 1 on one
-    amplified key, and bf16 outputs add O's output rounding to D (about 0.1 in
-    dQ)."""
-    joint_check(WORKLOADS["128k"], 0, n_random=8, hilo=bd.HILO_ALL)
+    that meets the bar there and that bench.py times: fp32 outputs and every P and dS
+    product in two bf16 terms on the tiles that hold a probability of 1/64 or more
+    (and, for comparison, on every tile).  Single terms fail in each kernel: P V and
+    dS K leave about 7e-2 in dQ (|dS| up to about 30, and D = rowsum(dO O) inherits
+    O's P rounding), P^T dO leaves 5.4e-2 in dV of a corrupted block whose queries
+    put P near 1 on one amplified key, and bf16 outputs add O's output rounding to D
+    (about 0.1 in dQ)."""
+    joint_check(WORKLOADS["128k"], 0, n_random=8, hilos=(HILO_128K, bd.HILO_ALL))
 
 
 def test_workload_128k_block_reading():
-    joint_check(WORKLOADS["128k"], 1, n_random=4, hilo=bd.HILO_ALL)
+    joint_check(WORKLOADS["128k"], 1, n_random=4, hilo=HILO_128K)
 
 
 def csbp_ranges(w):
