@@ -159,108 +159,117 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_kernel(const AttnArgs a) {
       lane_j = j;
     }
 
-    // S^T = K Q^T and dP^T = V dO^T: K and V rows 32u + l32 by row reads.
-    const uint32_t sb = lds_addr(lds + cur * STAGE);
-    const uint32_t zr = sb + yrow;
-    f32x16 sacc[2], dpacc[2];
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        sacc[u][i] = 0.f;
-        dpacc[u][i] = 0.f;
-      }
-    {
-      // K and V fragments are read LA steps ahead of their products (steps
-      // run over (u, s)); the scheduling fences keep the compiler from
-      // sinking each read down to the product that uses it.
-      constexpr int LA = 2, NS = 2 * KS;
-      bf16x8 kf[LA + 1], vf[LA + 1];
-      auto addr = [&](int n) { return (zr ^ (32u * (n % KS))) + (n / KS) * 32 * RB; };
-#pragma unroll
-      for (int n = 0; n < LA; ++n) {
-        kf[n] = lds_load16(addr(n));
-        vf[n] = lds_load16(addr(n) + TB);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int n = 0; n < NS; ++n) {
-        if (n + LA < NS) {
-          kf[(n + LA) % (LA + 1)] = lds_load16(addr(n + LA));
-          vf[(n + LA) % (LA + 1)] = lds_load16(addr(n + LA) + TB);
-        }
-        const int u = n / KS, s = n % KS;
-        sacc[u] = mfma32(kf[n % (LA + 1)], qf[s], sacc[u]);
-        dpacc[u] = mfma32(vf[n % (LA + 1)], df[s], dpacc[u]);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    }
-
+    // On a partly visible tile, a wave none of whose rows sees any of the
+    // tile's keys skips it (it still copies and meets the barrier).
+    bool skip = false;
     if (!(t >= f0 && t < f1)) {
-      const int base = a.kr[j].pos0 + t * BN + 4 * half - lane_lo;
+      const int kstart = a.kr[j].pos0 + t * BN - lane_lo;
+      skip = __builtin_amdgcn_ballot_w64(lane_w > 0 && kstart < lane_w && kstart + BN > 0) == 0;
+    }
+    if (!skip) {
+      // S^T = K Q^T and dP^T = V dO^T: K and V rows 32u + l32 by row reads.
+      const uint32_t sb = lds_addr(lds + cur * STAGE);
+      const uint32_t zr = sb + yrow;
+      f32x16 sacc[2], dpacc[2];
 #pragma unroll
       for (int u = 0; u < 2; ++u)
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          const int kk = base + u * 32 + (i >> 2) * 8 + (i & 3);
-          if ((unsigned)kk >= (unsigned)lane_w) sacc[u][i] = -INFINITY;
+          sacc[u][i] = 0.f;
+          dpacc[u][i] = 0.f;
         }
-    }
+      {
+        // K and V fragments are read LA steps ahead of their products (steps
+        // run over (u, s)); the scheduling fences keep the compiler from
+        // sinking each read down to the product that uses it.
+        constexpr int LA = 2, NS = 2 * KS;
+        bf16x8 kf[LA + 1], vf[LA + 1];
+        auto addr = [&](int n) { return (zr ^ (32u * (n % KS))) + (n / KS) * 32 * RB; };
+#pragma unroll
+        for (int n = 0; n < LA; ++n) {
+          kf[n] = lds_load16(addr(n));
+          vf[n] = lds_load16(addr(n) + TB);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int n = 0; n < NS; ++n) {
+          if (n + LA < NS) {
+            kf[(n + LA) % (LA + 1)] = lds_load16(addr(n + LA));
+            vf[(n + LA) % (LA + 1)] = lds_load16(addr(n + LA) + TB);
+          }
+          const int u = n / KS, s = n % KS;
+          sacc[u] = mfma32(kf[n % (LA + 1)], qf[s], sacc[u]);
+          dpacc[u] = mfma32(vf[n % (LA + 1)], df[s], dpacc[u]);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
 
-    // dS^T = P^T (dP^T - D) in the S^T register layout, rounded to bf16; HM 1
-    // adds dS - bf16(dS) as a second bf16 term on every tile, HM 2 on the
-    // 16-key chunks that hold a probability of at least hilo_tau.
-    bf16x8 dsb[4], dsl[4];
-    float cmax[4] = {0.f, 0.f, 0.f, 0.f};  // HM 2: largest P per 16-key chunk
+      if (!(t >= f0 && t < f1)) {
+        const int base = a.kr[j].pos0 + t * BN + 4 * half - lane_lo;
 #pragma unroll
-    for (int u = 0; u < 2; ++u)
+        for (int u = 0; u < 2; ++u)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float p = exp2f_fast(fmaf(sacc[u][i], c, -lse2));
-        const float ds = p * (dpacc[u][i] - dl);
-        const bf16 hi = to_bf16(ds);
-        dsb[u * 2 + (i >> 3)][i & 7] = hi;
-        if constexpr (HM != 0) dsl[u * 2 + (i >> 3)][i & 7] = to_bf16(ds - (float)hi);
-        if constexpr (HM == 2) cmax[u * 2 + (i >> 3)] = fmaxf(cmax[u * 2 + (i >> 3)], p);
+          for (int i = 0; i < 16; ++i) {
+            const int kk = base + u * 32 + (i >> 2) * 8 + (i & 3);
+            if ((unsigned)kk >= (unsigned)lane_w) sacc[u][i] = -INFINITY;
+          }
       }
 
-    // dQ^T[d][q] += sum_key K[key][d] dS[q][key]; key order per 16-key step as in the forward.
-    const uint32_t zt0 = sb + ytr0, zt1 = sb + ytr1;  // K tile by transpose reads
-    auto dsk = [&](const bf16x8 (&dd)[4]) __attribute__((always_inline)) {
+      // dS^T = P^T (dP^T - D) in the S^T register layout, rounded to bf16; HM 1
+      // adds dS - bf16(dS) as a second bf16 term on every tile, HM 2 on the
+      // 16-key chunks that hold a probability of at least hilo_tau.
+      bf16x8 dsb[4], dsl[4];
+      float cmax[4] = {0.f, 0.f, 0.f, 0.f};  // HM 2: largest P per 16-key chunk
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
+      for (int u = 0; u < 2; ++u)
 #pragma unroll
-        for (int d = 0; d < DT; ++d) {
-          const bf16x8 ka = cat(lds_read_tr_at((zt0 ^ (64u * d)) + u * 16 * RB),
-                                lds_read_tr_at((zt1 ^ (64u * d)) + u * 16 * RB));
-          acc[d] = mfma32(ka, dd[u], acc[d]);
+        for (int i = 0; i < 16; ++i) {
+          const float p = exp2f_fast(fmaf(sacc[u][i], c, -lse2));
+          const float ds = p * (dpacc[u][i] - dl);
+          const bf16 hi = to_bf16(ds);
+          dsb[u * 2 + (i >> 3)][i & 7] = hi;
+          if constexpr (HM != 0) dsl[u * 2 + (i >> 3)][i & 7] = to_bf16(ds - (float)hi);
+          if constexpr (HM == 2) cmax[u * 2 + (i >> 3)] = fmaxf(cmax[u * 2 + (i >> 3)], p);
         }
-      }
-    };
-    if constexpr (HM == 1) {
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-#pragma unroll
-        for (int d = 0; d < DT; ++d) {
-          const bf16x8 ka = cat(lds_read_tr_at((zt0 ^ (64u * d)) + u * 16 * RB),
-                                lds_read_tr_at((zt1 ^ (64u * d)) + u * 16 * RB));
-          acc[d] = mfma32(ka, dsb[u], acc[d]);
-          acc[d] = mfma32(ka, dsl[u], acc[d]);
-        }
-      }
-    } else {
-      dsk(dsb);
-      if constexpr (HM == 2) {
-        // second terms of the 16-key chunks holding a probability >= hilo_tau
-        // (K^T fragments re-read)
+
+      // dQ^T[d][q] += sum_key K[key][d] dS[q][key]; key order per 16-key step as in the forward.
+      const uint32_t zt0 = sb + ytr0, zt1 = sb + ytr1;  // K tile by transpose reads
+      auto dsk = [&](const bf16x8 (&dd)[4]) __attribute__((always_inline)) {
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          if (__builtin_amdgcn_ballot_w64(cmax[u] >= a.hilo_tau) != 0) {
 #pragma unroll
-            for (int d = 0; d < DT; ++d) {
-              const bf16x8 ka = cat(lds_read_tr_at((zt0 ^ (64u * d)) + u * 16 * RB),
-                                    lds_read_tr_at((zt1 ^ (64u * d)) + u * 16 * RB));
-              acc[d] = mfma32(ka, dsl[u], acc[d]);
+          for (int d = 0; d < DT; ++d) {
+            const bf16x8 ka = cat(lds_read_tr_at((zt0 ^ (64u * d)) + u * 16 * RB),
+                                  lds_read_tr_at((zt1 ^ (64u * d)) + u * 16 * RB));
+            acc[d] = mfma32(ka, dd[u], acc[d]);
+          }
+        }
+      };
+      if constexpr (HM == 1) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+#pragma unroll
+          for (int d = 0; d < DT; ++d) {
+            const bf16x8 ka = cat(lds_read_tr_at((zt0 ^ (64u * d)) + u * 16 * RB),
+                                  lds_read_tr_at((zt1 ^ (64u * d)) + u * 16 * RB));
+            acc[d] = mfma32(ka, dsb[u], acc[d]);
+            acc[d] = mfma32(ka, dsl[u], acc[d]);
+          }
+        }
+      } else {
+        dsk(dsb);
+        if constexpr (HM == 2) {
+          // second terms of the 16-key chunks holding a probability >= hilo_tau
+          // (K^T fragments re-read)
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            if (__builtin_amdgcn_ballot_w64(cmax[u] >= a.hilo_tau) != 0) {
+#pragma unroll
+              for (int d = 0; d < DT; ++d) {
+                const bf16x8 ka = cat(lds_read_tr_at((zt0 ^ (64u * d)) + u * 16 * RB),
+                                      lds_read_tr_at((zt1 ^ (64u * d)) + u * 16 * RB));
+                acc[d] = mfma32(ka, dsl[u], acc[d]);
+              }
             }
           }
         }

@@ -156,130 +156,139 @@ __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
       lane_j = j;
     }
 
-    // S^T = K Q^T: K rows 32u + l32 by row reads (K tile at the stage base).
-    const uint32_t sb = lds_addr(lds + cur * STAGE);
-    const uint32_t zr = sb + yrow;
-    f32x16 sacc[2];
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) sacc[u][i] = 0.f;
-    {
-      // K fragments are read LA k-steps ahead of their products; the
-      // scheduling fences keep the compiler from sinking each read down to
-      // the product that uses it (which left every MFMA waiting on an LDS
-      // read issued one product earlier).
-      constexpr int LA = 3;
-      bf16x8 kf[LA + 1][2];
-#pragma unroll
-      for (int s = 0; s < LA; ++s)
-#pragma unroll
-        for (int u = 0; u < 2; ++u) kf[s][u] = lds_load16((zr ^ (32u * s)) + u * 32 * RB);
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        if (s + LA < KS) {
-#pragma unroll
-          for (int u = 0; u < 2; ++u) kf[(s + LA) % (LA + 1)][u] = lds_load16((zr ^ (32u * (s + LA))) + u * 32 * RB);
-        }
-#pragma unroll
-        for (int u = 0; u < 2; ++u) sacc[u] = mfma32(kf[s % (LA + 1)][u], qf[s], sacc[u]);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    }
-
+    // On a partly visible tile, a wave none of whose rows sees any of the
+    // tile's keys skips it (it still copies and meets the barrier).
+    bool skip = false;
     if (!(t >= f0 && t < f1)) {
-      const int base = a.kr[j].pos0 + t * BN + 4 * half - lane_lo;
+      const int kstart = a.kr[j].pos0 + t * BN - lane_lo;
+      skip = __builtin_amdgcn_ballot_w64(lane_w > 0 && kstart < lane_w && kstart + BN > 0) == 0;
+    }
+    if (!skip) {
+      // S^T = K Q^T: K rows 32u + l32 by row reads (K tile at the stage base).
+      const uint32_t sb = lds_addr(lds + cur * STAGE);
+      const uint32_t zr = sb + yrow;
+      f32x16 sacc[2];
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) sacc[u][i] = 0.f;
+      {
+        // K fragments are read LA k-steps ahead of their products; the
+        // scheduling fences keep the compiler from sinking each read down to
+        // the product that uses it (which left every MFMA waiting on an LDS
+        // read issued one product earlier).
+        constexpr int LA = 3;
+        bf16x8 kf[LA + 1][2];
+#pragma unroll
+        for (int s = 0; s < LA; ++s)
+#pragma unroll
+          for (int u = 0; u < 2; ++u) kf[s][u] = lds_load16((zr ^ (32u * s)) + u * 32 * RB);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+          if (s + LA < KS) {
+#pragma unroll
+            for (int u = 0; u < 2; ++u) kf[(s + LA) % (LA + 1)][u] = lds_load16((zr ^ (32u * (s + LA))) + u * 32 * RB);
+          }
+#pragma unroll
+          for (int u = 0; u < 2; ++u) sacc[u] = mfma32(kf[s % (LA + 1)][u], qf[s], sacc[u]);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+
+      if (!(t >= f0 && t < f1)) {
+        const int base = a.kr[j].pos0 + t * BN + 4 * half - lane_lo;
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const int kk = base + u * 32 + (i >> 2) * 8 + (i & 3);
+            if ((unsigned)kk >= (unsigned)lane_w) sacc[u][i] = -INFINITY;
+          }
+      }
+
+      float mx = -INFINITY;
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[u][i]);
+      mx = fmaxf(mx, partner(mx));
+      // Lazy rescaling: the running max m_run only moves when some lane's tile
+      // max exceeds it by more than kSlack (log2 units).  Otherwise the stale
+      // max stays, so p = exp2(s c - m_run) <= 2^kSlack: exact in fp32 and bf16,
+      // and l_run, O and the final LSE all use the same m_run.  The test is
+      // wave-uniform, so the O rescale (64 multiplies per lane) is skipped for
+      // the whole wave on most tiles.
+      if (__builtin_amdgcn_ballot_w64(mx * c > m_run + kSlack) != 0) {
+        const float m_new = fmaxf(m_run, mx * c);
+        const float alpha = exp2f_fast(m_run - ((m_new == -INFINITY) ? 0.f : m_new));
+        l_run *= alpha;
+#pragma unroll
+        for (int d = 0; d < DT; ++d)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) acc[d][i] *= alpha;
+        m_run = m_new;
+      }
+      const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
+      float psum = 0.f;
+      // HM 2: a 16-key chunk of the tile also carries P - bf16(P) as a second
+      // bf16 term when some lane's largest p in it reaches hilo_tau times the
+      // lane's running sum.  The row sum only grows, so an element whose final
+      // probability reaches hilo_tau always passes this test.
+      bf16x8 pb[4], pl[4];
+      float cmax[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int u = 0; u < 2; ++u)
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          const int kk = base + u * 32 + (i >> 2) * 8 + (i & 3);
-          if ((unsigned)kk >= (unsigned)lane_w) sacc[u][i] = -INFINITY;
+          const float p = exp2f_fast(fmaf(sacc[u][i], c, -m_use));
+          psum += p;
+          const bf16 hi = to_bf16(p);
+          pb[u * 2 + (i >> 3)][i & 7] = hi;
+          if constexpr (HM != 0) pl[u * 2 + (i >> 3)][i & 7] = to_bf16(p - (float)hi);
+          if constexpr (HM == 2) cmax[u * 2 + (i >> 3)] = fmaxf(cmax[u * 2 + (i >> 3)], p);
         }
-    }
+      const float lim = a.hilo_tau * l_run;
+      l_run += psum;
 
-    float mx = -INFINITY;
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[u][i]);
-    mx = fmaxf(mx, partner(mx));
-    // Lazy rescaling: the running max m_run only moves when some lane's tile
-    // max exceeds it by more than kSlack (log2 units).  Otherwise the stale
-    // max stays, so p = exp2(s c - m_run) <= 2^kSlack: exact in fp32 and bf16,
-    // and l_run, O and the final LSE all use the same m_run.  The test is
-    // wave-uniform, so the O rescale (64 multiplies per lane) is skipped for
-    // the whole wave on most tiles.
-    if (__builtin_amdgcn_ballot_w64(mx * c > m_run + kSlack) != 0) {
-      const float m_new = fmaxf(m_run, mx * c);
-      const float alpha = exp2f_fast(m_run - ((m_new == -INFINITY) ? 0.f : m_new));
-      l_run *= alpha;
-#pragma unroll
-      for (int d = 0; d < DT; ++d)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) acc[d][i] *= alpha;
-      m_run = m_new;
-    }
-    const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
-    float psum = 0.f;
-    // HM 2: a 16-key chunk of the tile also carries P - bf16(P) as a second
-    // bf16 term when some lane's largest p in it reaches hilo_tau times the
-    // lane's running sum.  The row sum only grows, so an element whose final
-    // probability reaches hilo_tau always passes this test.
-    bf16x8 pb[4], pl[4];
-    float cmax[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int u = 0; u < 2; ++u)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float p = exp2f_fast(fmaf(sacc[u][i], c, -m_use));
-        psum += p;
-        const bf16 hi = to_bf16(p);
-        pb[u * 2 + (i >> 3)][i & 7] = hi;
-        if constexpr (HM != 0) pl[u * 2 + (i >> 3)][i & 7] = to_bf16(p - (float)hi);
-        if constexpr (HM == 2) cmax[u * 2 + (i >> 3)] = fmaxf(cmax[u * 2 + (i >> 3)], p);
-      }
-    const float lim = a.hilo_tau * l_run;
-    l_run += psum;
-
-    // O^T[d][q] += sum_key V[key][d] P[q][key]; the key order inside each
-    // 16-key step follows the S^T register layout (see device.hpp).
-    const uint32_t zt0 = sb + TB + ytr0, zt1 = sb + TB + ytr1;  // V tile by transpose reads
-    auto pv = [&](const bf16x8 (&pp)[4]) __attribute__((always_inline)) {
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-#pragma unroll
-        for (int d = 0; d < DT; ++d) {
-          const bf16x8 va = cat(lds_read_tr_at((zt0 ^ (64u * d)) + u * 16 * RB),
-                                lds_read_tr_at((zt1 ^ (64u * d)) + u * 16 * RB));
-          acc[d] = mfma32(va, pp[u], acc[d]);
-        }
-      }
-    };
-    if constexpr (HM == 1) {
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-#pragma unroll
-        for (int d = 0; d < DT; ++d) {
-          const bf16x8 va = cat(lds_read_tr_at((zt0 ^ (64u * d)) + u * 16 * RB),
-                                lds_read_tr_at((zt1 ^ (64u * d)) + u * 16 * RB));
-          acc[d] = mfma32(va, pb[u], acc[d]);
-          acc[d] = mfma32(va, pl[u], acc[d]);
-        }
-      }
-    } else {
-      pv(pb);
-      if constexpr (HM == 2) {
-        // second terms of the chunks that hold a large p (V^T fragments re-read)
+      // O^T[d][q] += sum_key V[key][d] P[q][key]; the key order inside each
+      // 16-key step follows the S^T register layout (see device.hpp).
+      const uint32_t zt0 = sb + TB + ytr0, zt1 = sb + TB + ytr1;  // V tile by transpose reads
+      auto pv = [&](const bf16x8 (&pp)[4]) __attribute__((always_inline)) {
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          if (__builtin_amdgcn_ballot_w64(cmax[u] >= lim) != 0) {
 #pragma unroll
-            for (int d = 0; d < DT; ++d) {
-              const bf16x8 va = cat(lds_read_tr_at((zt0 ^ (64u * d)) + u * 16 * RB),
-                                    lds_read_tr_at((zt1 ^ (64u * d)) + u * 16 * RB));
-              acc[d] = mfma32(va, pl[u], acc[d]);
+          for (int d = 0; d < DT; ++d) {
+            const bf16x8 va = cat(lds_read_tr_at((zt0 ^ (64u * d)) + u * 16 * RB),
+                                  lds_read_tr_at((zt1 ^ (64u * d)) + u * 16 * RB));
+            acc[d] = mfma32(va, pp[u], acc[d]);
+          }
+        }
+      };
+      if constexpr (HM == 1) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+#pragma unroll
+          for (int d = 0; d < DT; ++d) {
+            const bf16x8 va = cat(lds_read_tr_at((zt0 ^ (64u * d)) + u * 16 * RB),
+                                  lds_read_tr_at((zt1 ^ (64u * d)) + u * 16 * RB));
+            acc[d] = mfma32(va, pb[u], acc[d]);
+            acc[d] = mfma32(va, pl[u], acc[d]);
+          }
+        }
+      } else {
+        pv(pb);
+        if constexpr (HM == 2) {
+          // second terms of the chunks that hold a large p (V^T fragments re-read)
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            if (__builtin_amdgcn_ballot_w64(cmax[u] >= lim) != 0) {
+#pragma unroll
+              for (int d = 0; d < DT; ++d) {
+                const bf16x8 va = cat(lds_read_tr_at((zt0 ^ (64u * d)) + u * 16 * RB),
+                                      lds_read_tr_at((zt1 ^ (64u * d)) + u * 16 * RB));
+                acc[d] = mfma32(va, pl[u], acc[d]);
+              }
             }
           }
         }
