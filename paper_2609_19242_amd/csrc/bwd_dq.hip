@@ -176,7 +176,7 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_kernel(const AttnArgs a) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           sacc[u][i] = 0.f;
-          dpacc[u][i] = 0.f;
+          dpacc[u][i] = -dl;  // dP^T - D accumulates from -D (one subtract less per score)
         }
       {
         // K and V fragments are read LA steps ahead of their products (steps
@@ -225,7 +225,7 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_kernel(const AttnArgs a) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const float p = exp2f_fast(fmaf(sacc[u][i], c, -lse2));
-          const float ds = p * (dpacc[u][i] - dl);
+          const float ds = p * dpacc[u][i];
           const bf16 hi = to_bf16(ds);
           dsb[u * 2 + (i >> 3)][i & 7] = hi;
           if constexpr (HM != 0) dsl[u * 2 + (i >> 3)][i & 7] = to_bf16(ds - (float)hi);
