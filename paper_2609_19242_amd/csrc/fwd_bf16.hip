@@ -27,7 +27,7 @@ namespace bdlm {
 namespace {
 
 constexpr float kLn2 = 0.69314718055994530942f;
-constexpr float kSlack = 8.f;  // largest exponent p = exp2(s c - m_run) may reach before m_run moves
+constexpr float kSumLimit = 18446744073709551616.f;  // 2^64: a lane's tile sum of p above which m_run moves
 
 template <int D, int NW, int HM>
 __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
@@ -207,19 +207,48 @@ __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
           }
       }
 
-      float mx = -INFINITY;
+      // HM 2: a 16-key chunk of the tile also carries P - bf16(P) as a second
+      // bf16 term when some lane's largest p in it reaches hilo_tau times the
+      // lane's running sum.  The row sum only grows, so an element whose final
+      // probability reaches hilo_tau always passes this test.
+      float psum;
+      bf16x8 pb[4], pl[4];
+      float cmax[4];
+      auto probs = [&](float m_use) __attribute__((always_inline)) {
+        psum = 0.f;
 #pragma unroll
-      for (int u = 0; u < 2; ++u)
+        for (int k = 0; k < 4; ++k) cmax[k] = 0.f;
 #pragma unroll
-        for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[u][i]);
-      mx = fmaxf(mx, partner(mx));
-      // Lazy rescaling: the running max m_run only moves when some lane's tile
-      // max exceeds it by more than kSlack (log2 units).  Otherwise the stale
-      // max stays, so p = exp2(s c - m_run) <= 2^kSlack: exact in fp32 and bf16,
-      // and l_run, O and the final LSE all use the same m_run.  The test is
-      // wave-uniform, so the O rescale (64 multiplies per lane) is skipped for
-      // the whole wave on most tiles.
-      if (__builtin_amdgcn_ballot_w64(mx * c > m_run + kSlack) != 0) {
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const float p = exp2f_fast(fmaf(sacc[u][i], c, -m_use));
+            psum += p;
+            const bf16 hi = to_bf16(p);
+            pb[u * 2 + (i >> 3)][i & 7] = hi;
+            if constexpr (HM != 0) pl[u * 2 + (i >> 3)][i & 7] = to_bf16(p - (float)hi);
+            if constexpr (HM == 2) cmax[u * 2 + (i >> 3)] = fmaxf(cmax[u * 2 + (i >> 3)], p);
+          }
+      };
+      // Lazy rescaling: the running max m_run of a row moves only on the row's
+      // first visible tile or when p = exp2(s c - m_run) summed over a lane's
+      // part of the tile exceeds 2^64; the tile max is computed only then.
+      // Otherwise the stale max stays (every p <= 2^64: no overflow in fp32
+      // or bf16, and l_run, O and the final LSE all use the same m_run).  The
+      // tests are wave-uniform, so the O rescale (64 multiplies per lane) and
+      // the max are skipped for the whole wave on almost every tile.
+      bool rescale = __builtin_amdgcn_ballot_w64(m_run == -INFINITY) != 0;
+      if (!rescale) {
+        probs(m_run);
+        rescale = __builtin_amdgcn_ballot_w64(psum > kSumLimit) != 0;
+      }
+      if (rescale) {
+        float mx = -INFINITY;
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sacc[u][i]);
+        mx = fmaxf(mx, partner(mx));
         const float m_new = fmaxf(m_run, mx * c);
         const float alpha = exp2f_fast(m_run - ((m_new == -INFINITY) ? 0.f : m_new));
         l_run *= alpha;
@@ -228,26 +257,8 @@ __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
 #pragma unroll
           for (int i = 0; i < 16; ++i) acc[d][i] *= alpha;
         m_run = m_new;
+        probs((m_run == -INFINITY) ? 0.f : m_run);
       }
-      const float m_use = (m_run == -INFINITY) ? 0.f : m_run;
-      float psum = 0.f;
-      // HM 2: a 16-key chunk of the tile also carries P - bf16(P) as a second
-      // bf16 term when some lane's largest p in it reaches hilo_tau times the
-      // lane's running sum.  The row sum only grows, so an element whose final
-      // probability reaches hilo_tau always passes this test.
-      bf16x8 pb[4], pl[4];
-      float cmax[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int u = 0; u < 2; ++u)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const float p = exp2f_fast(fmaf(sacc[u][i], c, -m_use));
-          psum += p;
-          const bf16 hi = to_bf16(p);
-          pb[u * 2 + (i >> 3)][i & 7] = hi;
-          if constexpr (HM != 0) pl[u * 2 + (i >> 3)][i & 7] = to_bf16(p - (float)hi);
-          if constexpr (HM == 2) cmax[u * 2 + (i >> 3)] = fmaxf(cmax[u * 2 + (i >> 3)], p);
-        }
       const float lim = a.hilo_tau * l_run;
       l_run += psum;
 
