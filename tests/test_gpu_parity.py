@@ -6,6 +6,8 @@ backward key tiles, 32-row backward query steps); they cover both readings of
 the clean-to-clean rule, GQA groups, head_dim 64 and 128, batch > 1, the
 degenerate block sizes (1 and L) and rows that see no key.
 """
+import math
+
 import numpy as np
 import pytest
 import torch
@@ -102,6 +104,33 @@ def test_two_terms_amplified_keys(reading, hilo, Hq):
     do = synth.normal((1, 2 * L, Hq, D), 9103, torch.bfloat16)
     h = bd.HILO_ALL | (bd.HILO_ADAPTIVE if hilo == "adaptive" else 0)
     check_joint(q, k, v, do, M, reading, torch.bfloat16, tag=f"amplified {hilo} H{Hq} r{reading}", hilo=h)
+
+
+@pytest.mark.parametrize("hilo", ["single", "adaptive"])
+def test_forward_running_max_moves_mid_walk(hilo):
+    """Scores that grow along the key positions (about 12 log2 units per 64-key tile,
+    over 190 across the sequence), so the forward's running max moves several times
+    inside a row's walk (the lazy rescale of O and of the row sum), not only on the
+    row's first tile: O and LSE of every row against the oracle, batch 1,
+    L = 1024 + 1024, block 32, 2/1 heads, d 128, fp32 outputs."""
+    import synth
+    L, M, Hq, Hkv, D = 1024, 32, 2, 1, 128
+    q = synth.normal((1, 2 * L, Hq, D), 9200, torch.float32)
+    q[..., 0] = 20.0
+    k = synth.normal((1, 2 * L, Hkv, D), 9201, torch.float32) * 0.1
+    ramp = 0.075 * torch.arange(L, dtype=torch.float32)
+    k[0, :L, 0, 0] = ramp  # corrupted stream
+    k[0, L:, 0, 0] = ramp  # clean stream
+    q, k = q.to(torch.bfloat16), k.to(torch.bfloat16)
+    v = synth.normal((1, 2 * L, Hkv, D), 9202, torch.bfloat16)
+    s2 = (k[0, L:, 0].double() @ q[0, -1, 0].double()) / math.sqrt(D) * math.log2(math.e)
+    assert float(s2.max() - s2.min()) > 3 * 64, "the test needs several moves of the running max"
+    h = 0 if hilo == "single" else bd.HILO_ALL | bd.HILO_ADAPTIVE
+    o, lse = bd.joint_fwd(q.to(DEV), k.to(DEV), v.to(DEV), M, out_f32=True, hilo=h)
+    torch.cuda.synchronize()
+    O, LSE = oracle.joint_fwd(q, k, v, L, M)
+    assert_close(f"rising scores {hilo} O", o, O, torch.bfloat16)
+    assert_close(f"rising scores {hilo} LSE", lse, LSE, torch.bfloat16)
 
 
 @pytest.mark.parametrize("reading", [0, 1], ids=["causal", "block"])
