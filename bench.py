@@ -6,7 +6,8 @@ L = 32768 clean + 32768 corrupted tokens, block size 64, 32 query / 8 KV heads,
 head_dim 128, bf16 inputs, fp32 accumulation, bf16 outputs), seeded synthetic
 N(0, 1) inputs resident in HBM before the timed region.  One step = one
 bdlm_attn_fwd + one bdlm_attn_bwd call (tile classification, fused forward,
-backward pre-pass, the key-major dK/dV kernel and the query-major dQ kernel).
+the query-major dQ kernel, which also forms D = rowsum(dO * O), and the
+key-major dK/dV kernel).
 
 value = useful TFLOP/s: valid query-key pairs of the mask (the paper's unit of
 attention work, App. B) x (4 d forward + 10 d backward) FLOP, divided by the

@@ -458,9 +458,13 @@ bdlm_status attn_bwd_impl(const bdlm_problem* p, int32_t n_q, const bdlm_range* 
       a.order[n++] = best;
     }
   }
-  hipError_t e = timed(kKBwdPre, stream, [&] { return launch_bwd_pre(a, p->head_dim, p->dtype, stream); });
-  if (e != hipSuccess) return hip_fail(e, "backward pre-pass launch");
+  hipError_t e = hipSuccess;
   if (p->dtype == BDLM_BF16) {
+    // The dQ kernel computes D = rowsum(dO * O) itself and leaves each row's
+    // statistics in the workspace for the dK/dV kernel, so it runs first.
+    for (int j = 0; j < n_k; ++j) aq.order[j] = a.order[j];
+    e = timed(kKBwdDq, stream, [&] { return launch_bwd_dq_bf16(aq, p->head_dim, stream); });
+    if (e != hipSuccess) return hip_fail(e, "backward dQ launch");
     e = timed(kKBwdBf16, stream, [&] {
       if (!a.stats_form) return launch_bwd_bf16(a, p->head_dim, stream);
       // The scheduled kernel walks at most two query ranges: pass it the ranges
@@ -472,10 +476,9 @@ bdlm_status attn_bwd_impl(const bdlm_problem* p, int32_t n_q, const bdlm_range* 
       return launch_bwd_dkdv(ak, stream);
     });
     if (e != hipSuccess) return hip_fail(e, "backward dK/dV launch");
-    for (int j = 0; j < n_k; ++j) aq.order[j] = a.order[j];
-    e = timed(kKBwdDq, stream, [&] { return launch_bwd_dq_bf16(aq, p->head_dim, stream); });
-    if (e != hipSuccess) return hip_fail(e, "backward dQ launch");
   } else {
+    e = timed(kKBwdPre, stream, [&] { return launch_bwd_pre(a, p->head_dim, stream); });
+    if (e != hipSuccess) return hip_fail(e, "backward pre-pass launch");
     e = timed(kKBwdF32, stream, [&] { return launch_bwd_f32(a, p->head_dim, stream); });
     if (e != hipSuccess) return hip_fail(e, "backward launch");
   }

@@ -27,15 +27,15 @@
 // branch-free, and empty asm statements pin its scalar work to its place in
 // the order (the compiler would otherwise hoist it to the top of the step,
 // where nothing overlaps it).
-// S and dP accumulate on top of -LSE/scale and -D read from LDS (the pre-pass
-// writes that form), so the softmax is one multiply and one exp2 per score
-// and dS one multiply; rows the mask hides start at -inf.  LDS holds four
-// stages, filled by LDS-DMA copies three steps ahead, so the next step's
-// data is resident while a step runs; the copies are issued as inline
-// assembly, which keeps the compiler from waiting on them before every LDS
-// transpose read (it cannot tell which stage a DMA writes).  The dV/dK
-// products are inline-assembly MFMAs on AGPR accumulators (the S/dP products
-// use VGPR accumulators, which the softmax reads).
+// S and dP accumulate on top of -LSE/scale and -D read from LDS (the dQ
+// kernel, which runs first, writes that form), so the softmax is one multiply
+// and one exp2 per score and dS one multiply; rows the mask hides start at
+// -inf.  LDS holds four stages, filled by LDS-DMA copies three steps ahead,
+// so the next step's data is resident while a step runs; the copies are
+// issued as inline assembly, which keeps the compiler from waiting on them
+// before every LDS transpose read (it cannot tell which stage a DMA writes).
+// The dV/dK products are inline-assembly MFMAs on AGPR accumulators (the S/dP
+// products use VGPR accumulators, which the softmax reads).
 #include "common.hpp"
 #include "device.hpp"
 

@@ -44,8 +44,11 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_kernel(const AttnArgs a) {
   const int nvalid = imin(BM, qr.len - row0);
   const int64_t H = a.heads;
 
-  // This wave's 32 query rows of Q and dO as MFMA B fragments.
+  // This wave's 32 query rows of Q and dO as MFMA B fragments, and
+  // D = rowsum(dO * O) of the lane's row: a lane holds half of the row's
+  // elements (8-element chunks 2s + half), its partner lane the other half.
   bf16x8 qf[KS], df[KS];
+  float dsum = 0.f;
   {
     const int64_t qoff = (((int64_t)it.b * qr.bstride + row0) * H + it.h) * D;
     const uint32_t bytes = (uint32_t)(((int64_t)(nvalid - 1) * H * D + D) * 2);
@@ -57,18 +60,52 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_kernel(const AttnArgs a) {
       qf[s] = __builtin_bit_cast(bf16x8, buf_load16(rq, off + s * 32));
       df[s] = __builtin_bit_cast(bf16x8, buf_load16(rdo, off + s * 32));
     }
+    if (a.out_f32) {  // O in fp32: two 16-byte loads per chunk
+      const auto ro = make_rsrc((const float*)qr.o + qoff, 2 * bytes);
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        const f32x4 o0 = __builtin_bit_cast(f32x4, buf_load16(ro, 2 * off + s * 64));
+        const f32x4 o1 = __builtin_bit_cast(f32x4, buf_load16(ro, 2 * off + s * 64 + 16));
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          dsum = fmaf(o0[e], (float)df[s][e], dsum);
+          dsum = fmaf(o1[e], (float)df[s][4 + e], dsum);
+        }
+      }
+    } else {
+      const auto ro = make_rsrc((const bf16*)qr.o + qoff, bytes);
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        const bf16x8 o = __builtin_bit_cast(bf16x8, buf_load16(ro, off + s * 32));
+#pragma unroll
+        for (int e = 0; e < 8; ++e) dsum = fmaf((float)o[e], (float)df[s][e], dsum);
+      }
+    }
   }
+  dsum += partner(dsum);
   const int my_row = row0 + w * 32 + l32;
   const bool row_ok = my_row < qr.len;
   const int pq = qr.pos0 + imin(my_row, qr.len - 1);
   const int pq0 = qr.pos0 + row0, pq1 = qr.pos0 + row0 + nvalid - 1;
-  // Rows past the range and rows that see no key get P = 0.
-  float lse2 = INFINITY, dl = 0.f;
+  // Rows past the range and rows that see no key get P = 0.  The row's
+  // statistics for the dK/dV kernel, which runs after this one, go to the
+  // workspace: (LSE log2(e), D), or (-LSE / scale, -D) for the scheduled
+  // kernel (stats form 1).
+  float lse2 = INFINITY;
+  const float dl = dsum;
   if (row_ok) {
     const float z = qr.lse[((int64_t)it.b * H + it.h) * qr.bstride + my_row];
     lse2 = (z == -INFINITY) ? INFINITY : z * kLog2e;
-    dl = qr.delta[((int64_t)it.b * H + it.h) * qr.len + my_row];
-    if (a.stats_form) dl = -dl;  // the workspace holds -D
+    if (half == 0) {
+      const int64_t si = ((int64_t)it.b * H + it.h) * qr.len + my_row;
+      if (a.stats_form) {
+        qr.delta[si] = -dsum;
+        qr.l2[si] = (z == -INFINITY) ? -INFINITY : -z / a.scale;
+      } else {
+        qr.delta[si] = dsum;
+        qr.l2[si] = (z == -INFINITY) ? INFINITY : z * kLog2e;
+      }
+    }
   }
 
   f32x16 acc[DT];

@@ -1,16 +1,12 @@
-// Backward pre-pass, gfx950 (an HBM-bound elementwise pass).
+// Backward pre-pass of the fp32 path, gfx950 (an HBM-bound elementwise pass).
 //
 // D[b][h][row] = sum_d dO * O in fp32: the row dot the softmax gradient
-// dS = P * (dP - D) needs (arXiv 2609.19242 App. C reuses the saved O), and a
-// per-row form of LSE for the dK/dV kernel, in one of two forms:
-//  * form 0: L2 = LSE * log2(e) (+inf for rows that see no key, so that
-//    exp2(s - L2) is 0 for them) and D;
-//  * form 1: -LSE / scale (-inf for rows that see no key) and -D, the values
-//    the scheduled dK/dV kernel starts its score and dP accumulators at, so
-//    that P = exp2(scale log2(e) acc) and dS = P acc' need no subtraction.
-// One thread per 8 consecutive head_dim elements; the D/8 threads of one
-// (row, head) are adjacent lanes and reduce with cross-lane shuffles.  O and
-// dO are read once, with the non-temporal cache policy.
+// dS = P * (dP - D) needs (arXiv 2609.19242 App. C reuses the saved O), and
+// L2 = LSE * log2(e) (+inf for rows that see no key, so that exp2(s - L2) is 0
+// for them), the per-row values the fp32 backward kernel reads.  (The bf16
+// path computes D inside its dQ kernel.)  One thread per 8 consecutive
+// head_dim elements; the D/8 threads of one (row, head) are adjacent lanes and
+// reduce with cross-lane shuffles.
 #include "common.hpp"
 #include "device.hpp"
 
@@ -18,7 +14,7 @@ namespace bdlm {
 
 namespace {
 
-template <int D, typename T, typename TO>
+template <int D>
 __global__ __launch_bounds__(256) void bwd_pre_kernel(const AttnArgs a) {
   constexpr int CPR = D / 8;
   const QRangeArg& qr = a.qr[blockIdx.y];
@@ -36,23 +32,8 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(const AttnArgs a) {
   const int64_t off = ((b * qr.bstride + row) * H + h) * D + chunk * 8;
   float s = 0.f;
   if (ok) {
-    float o[8], d[8];
-    if constexpr (sizeof(TO) == 2) {
-      const bf16x8 x = __builtin_bit_cast(bf16x8, __builtin_nontemporal_load((const u32x4*)((const bf16*)qr.o + off)));
-#pragma unroll
-      for (int e = 0; e < 8; ++e) o[e] = (float)x[e];
-    } else {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) o[e] = ((const float*)qr.o)[off + e];
-    }
-    if constexpr (sizeof(T) == 2) {
-      const bf16x8 x = __builtin_bit_cast(bf16x8, __builtin_nontemporal_load((const u32x4*)((const bf16*)qr.dO + off)));
-#pragma unroll
-      for (int e = 0; e < 8; ++e) d[e] = (float)x[e];
-    } else {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) d[e] = ((const float*)qr.dO)[off + e];
-    }
+    const float* o = (const float*)qr.o + off;
+    const float* d = (const float*)qr.dO + off;
 #pragma unroll
     for (int e = 0; e < 8; ++e) s = fmaf(o[e], d[e], s);
   }
@@ -61,13 +42,8 @@ __global__ __launch_bounds__(256) void bwd_pre_kernel(const AttnArgs a) {
   if (!ok) return;
   if (chunk == 0) {
     const float z = qr.lse[(b * H + h) * qr.bstride + row];
-    if (a.stats_form) {
-      qr.delta[(b * H + h) * qr.len + row] = -s;
-      qr.l2[(b * H + h) * qr.len + row] = (z == -INFINITY) ? -INFINITY : -z / a.scale;
-    } else {
-      qr.delta[(b * H + h) * qr.len + row] = s;
-      qr.l2[(b * H + h) * qr.len + row] = (z == -INFINITY) ? INFINITY : z * 1.44269504088896340736f;
-    }
+    qr.delta[(b * H + h) * qr.len + row] = s;
+    qr.l2[(b * H + h) * qr.len + row] = (z == -INFINITY) ? INFINITY : z * 1.44269504088896340736f;
   }
 }
 
@@ -82,20 +58,12 @@ int64_t max_q_threads(const AttnArgs& a, int cpr) {
 
 }  // namespace
 
-hipError_t launch_bwd_pre(const AttnArgs& a, int head_dim, int dtype, hipStream_t s) {
+hipError_t launch_bwd_pre(const AttnArgs& a, int head_dim, hipStream_t s) {
   const int64_t t = max_q_threads(a, head_dim / 8);
   if (t == 0) return hipSuccess;
   const dim3 grid((unsigned)((t + 255) / 256), a.n_q);
-  if (dtype == 0 && !a.out_f32) {
-    if (head_dim == 128) hipLaunchKernelGGL((bwd_pre_kernel<128, bf16, bf16>), grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((bwd_pre_kernel<64, bf16, bf16>), grid, dim3(256), 0, s, a);
-  } else if (dtype == 0) {
-    if (head_dim == 128) hipLaunchKernelGGL((bwd_pre_kernel<128, bf16, float>), grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((bwd_pre_kernel<64, bf16, float>), grid, dim3(256), 0, s, a);
-  } else {
-    if (head_dim == 128) hipLaunchKernelGGL((bwd_pre_kernel<128, float, float>), grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL((bwd_pre_kernel<64, float, float>), grid, dim3(256), 0, s, a);
-  }
+  if (head_dim == 128) hipLaunchKernelGGL((bwd_pre_kernel<128>), grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL((bwd_pre_kernel<64>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -194,7 +194,7 @@ __device__ inline int xcd_remap(int wg, int n) {
 hipError_t launch_fwd_bf16(const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_fwd_f32(const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_merge(const MergeArgs& a, int head_dim, int part_dtype, int out_dtype, hipStream_t s);
-hipError_t launch_bwd_pre(const AttnArgs& a, int head_dim, int dtype, hipStream_t s);
+hipError_t launch_bwd_pre(const AttnArgs& a, int head_dim, hipStream_t s);  // fp32 path
 hipError_t launch_bwd_bf16(const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_bwd_dkdv(const AttnArgs& a, hipStream_t s);
 hipError_t launch_bwd_dq_bf16(const AttnArgs& a, int head_dim, hipStream_t s);
