@@ -33,13 +33,14 @@ def sorted_anchors(nblk, L, seed, n_used=None):
     return torch.cat([a, torch.full((nblk - n_used,), L)]).to(torch.int32)
 
 
-def check_joint_ext(q, k, v, do, M, reading, dtype, window=0, prefix=None, heads=None, tag=""):
+def check_joint_ext(q, k, v, do, M, reading, dtype, window=0, prefix=None, heads=None, tag="", hilo=0):
     L = q.shape[1] // 2
     qd, kd, vd, dod = (t.to(DEV) for t in (q, k, v, do))
     pref_d = prefix.to(DEV) if prefix is not None else None
-    o, lse = bd.joint_fwd(qd, kd, vd, M, clean_intra=reading, out_f32=True, window=window, clean_prefix=pref_d)
+    o, lse = bd.joint_fwd(qd, kd, vd, M, clean_intra=reading, out_f32=True, window=window, clean_prefix=pref_d,
+                          hilo=hilo)
     dq, dk, dv = bd.joint_bwd(qd, kd, vd, o, lse, dod, M, clean_intra=reading, out_f32=True, window=window,
-                              clean_prefix=pref_d)
+                              clean_prefix=pref_d, hilo=hilo)
     torch.cuda.synchronize()
     hs = list(range(q.shape[2])) if heads is None else heads
     pl = None if prefix is None else prefix.tolist()
@@ -69,14 +70,20 @@ WINDOW_CASES = [
 ]
 
 
-@pytest.mark.parametrize("dt", ["bf16", "fp32"])
+# bf16 with adaptive two-term P and dS products: the wave-level tile skip and
+# the adaptive selection on the same partly visible window tiles
+HILO_OF_DT = {"bf16-adaptive": bd.HILO_ALL | bd.HILO_ADAPTIVE}
+
+
+@pytest.mark.parametrize("dt", ["bf16", "bf16-adaptive", "fp32"])
 @pytest.mark.parametrize("reading", [0, 1], ids=["causal", "block"])
 @pytest.mark.parametrize("case", WINDOW_CASES, ids=lambda c: "L{}-M{}-H{}x{}-d{}-b{}-W{}".format(*c))
 def test_window_small(case, reading, dt):
     L, M, Hq, Hkv, D, B, W = case
     dtype = torch.float32 if dt == "fp32" else torch.bfloat16
     q, k, v, do = joint_inputs(L, Hq, Hkv, D, dtype, batch=B, seed=L + W)
-    check_joint_ext(q, k, v, do, M, reading, dtype, window=W, tag=f"L{L} M{M} W{W} r{reading}")
+    check_joint_ext(q, k, v, do, M, reading, dtype, window=W, tag=f"L{L} M{M} W{W} r{reading} {dt}",
+                    hilo=HILO_OF_DT.get(dt, 0))
 
 
 @pytest.mark.parametrize("dt", ["bf16", "fp32"])
@@ -103,11 +110,11 @@ def drafter_case(T, M, n_blocks, Hq, Hkv, D, dtype, seed, window=0):
     return q, kd_, vd_, kt, vt, do, prefix
 
 
-def check_drafter(T, M, n_blocks, Hq, Hkv, D, dtype, seed, heads=None, window=0):
+def check_drafter(T, M, n_blocks, Hq, Hkv, D, dtype, seed, heads=None, window=0, hilo=0):
     q, kd_, vd_, kt, vt, do, prefix = drafter_case(T, M, n_blocks, Hq, Hkv, D, dtype, seed, window)
     nd = n_blocks * M
     pref_d = prefix.to(DEV)
-    p = bd.make_problem(1, T, M, Hq, Hkv, D, dtype, out_f32=True, window=window, clean_prefix=pref_d)
+    p = bd.make_problem(1, T, M, Hq, Hkv, D, dtype, out_f32=True, window=window, clean_prefix=pref_d, hilo=hilo)
     qr = [Range(CORRUPTED, 0, nd)]
     kr = [Range(CORRUPTED, 0, nd), Range(CLEAN, 0, T)]
     qg, dog = q.to(DEV), do.to(DEV)
@@ -141,11 +148,11 @@ def check_drafter(T, M, n_blocks, Hq, Hkv, D, dtype, seed, heads=None, window=0)
     assert bd.visible_pairs(p, qr, kr) == oracle.count_visible_pairs(oq, ok, M, window=window, clean_prefix=pl)
 
 
-@pytest.mark.parametrize("dt", ["bf16", "fp32"])
+@pytest.mark.parametrize("dt", ["bf16", "bf16-adaptive", "fp32"])
 @pytest.mark.parametrize("window", [0, 70])
 def test_drafter_small(window, dt):
     dtype = torch.float32 if dt == "fp32" else torch.bfloat16
-    check_drafter(608, 16, 24, 4, 2, 128, dtype, seed=13, window=window)
+    check_drafter(608, 16, 24, 4, 2, 128, dtype, seed=13, window=window, hilo=HILO_OF_DT.get(dt, 0))
 
 
 def test_two_complementary_views_are_batch_elements():
