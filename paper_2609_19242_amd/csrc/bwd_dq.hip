@@ -10,7 +10,10 @@
 // as A operands, the wave's Q and dO rows in registers as B operands), P and dS
 // in registers (a lane owns one query row, so its LSE and D are scalars), and
 // dQ^T += K^T dS^T with K^T read from the row-major K tile by LDS transpose
-// reads, the same product shape as the forward's O^T += V^T P^T.
+// reads, the same product shape as the forward's O^T += V^T P^T.  The kernel
+// forms D_i = dO_i . O_i itself (the lane already holds half of dO_i) and
+// leaves each row's statistics in the workspace for the dK/dV kernel, which
+// runs after it.
 #include "qtiles.hpp"
 
 namespace bdlm {

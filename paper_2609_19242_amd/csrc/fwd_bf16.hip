@@ -9,12 +9,15 @@
 // Per key tile (BN = 64 keys) each wave computes S^T = K Q^T with
 // v_mfma_f32_32x32x16_bf16 (K from LDS as the A operand, the wave's Q rows held
 // in registers as B), so a lane owns one query row and 32 of the tile's keys;
-// the row max needs one permlane32 swap and the row sum stays split across the
-// two half-waves until the epilogue.  O^T += V^T P^T uses the probabilities
-// straight from the S^T registers as the B operand, and V^T fragments come
-// from the row-major V tile through LDS transpose reads.  K/V tiles are
-// double-buffered in LDS with one barrier per tile, K and V at the row pitches
-// that make their row reads and transpose reads free of bank conflicts.
+// the row max (needed only when the lazily kept running max moves) takes one
+// permlane32 swap and the row sum stays split across the two half-waves until
+// the epilogue.  O^T += V^T P^T uses the probabilities straight from the S^T
+// registers as the B operand, and V^T fragments come from the row-major V tile
+// through LDS transpose reads.  K/V tiles arrive by LDS-DMA copies two tiles
+// ahead into three stages, one barrier per tile, their rows stored unpadded
+// with a row-dependent XOR permutation of 16-byte chunks under which both the
+// row reads and the transpose reads are free of bank conflicts.  A wave none
+// of whose rows sees a partly visible tile skips it.
 //
 // Masking: each lane's visible keys in a key range are one position interval
 // (the rules in common.hpp).  Tiles inside every lane's interval run without a
