@@ -105,7 +105,7 @@ __device__ __forceinline__ f32x4 lds_f4(uint32_t a) {
 
 // ADAPT: a step also carries P - bf16(P) and dS - bf16(dS) of a head's
 // 16-row half as second bf16 terms when some probability of that half reaches
-// hilo_tau (8 more products: head 0's after block B, head 1's inside block D,
+// hilo_tau (8 more products: head 0's after block B, head 1's after block D,
 // each while its P and dS are still in registers).
 template <bool ADAPT>
 __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
