@@ -51,13 +51,36 @@ KERNEL_SOURCES = {
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_32k.json")
 
 
+def strip_comments(src):
+    """C++ source without its comments and blank lines (a comment edit leaves the hash alone)."""
+    out, i, n = [], 0, len(src)
+    while i < n:
+        c = src[i]
+        if c == '"':  # string literal, copied whole
+            j = i + 1
+            while j < n and src[j] != '"':
+                j += 2 if src[j] == "\\" else 1
+            out.append(src[i:j + 1])
+            i = j + 1
+        elif src.startswith("//", i):
+            j = src.find("\n", i)
+            i = n if j < 0 else j
+        elif src.startswith("/*", i):
+            j = src.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+        else:
+            out.append(c)
+            i += 1
+    return "\n".join(ln.rstrip() for ln in "".join(out).splitlines() if ln.strip())
+
+
 def kernel_source_hash(kernel):
-    """Hash of a kernel's sources and of their per-source compile options."""
+    """Hash of a kernel's sources (comments stripped) and of their per-source compile options."""
     from paper_2609_19242_amd import build
     h = hashlib.sha256()
     for f in KERNEL_SOURCES.get(kernel, []):
-        with open(os.path.join(ROOT, "paper_2609_19242_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, "paper_2609_19242_amd", "csrc", f), encoding="utf-8") as fh:
+            h.update(strip_comments(fh.read()).encode())
         h.update(" ".join(build.EXTRA_FLAGS.get(f, [])).encode())
     return h.hexdigest()[:16]
 
