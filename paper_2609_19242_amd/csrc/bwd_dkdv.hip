@@ -330,6 +330,10 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
   asm volatile("" : "+v"(ystat));  // one base register; stage, head and row offsets stay immediate
 
   f32x16 sa[NH], da[NH];
+  // The first row-read pairs of a step, issued at the end of the step before
+  // (its stage is complete from the barrier before that step on).
+  constexpr int RA = 4;  // row-read pairs in flight ahead of the score products
+  bf16x8 nq[RA], nd[RA];
   // Load the starts of step `cu` (stage st) and apply the mask of partly visible steps.
   auto load_starts = [&](int st, const Cursor cu) __attribute__((always_inline)) {
     const uint32_t base = ystat + st * kStatB;
@@ -414,7 +418,6 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
   // One step on stage ST: the copies of step `cp` into stage CP go out under
   // its first products, the starts of step `nx` (stage NX) are loaded under its
   // last ones, and the walk advances under the softmax of head 0.
-  constexpr int RA = 4;  // row-read pairs in flight ahead of the score products
   constexpr int TA = 4;  // transpose-read pairs in flight ahead of the dV/dK products
   Cursor c0, c1, c2, c3;
   CopyPlan cpl;  // copies of step c3, planned during the step before
@@ -428,10 +431,21 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
     auto rowd = [&](int n) { return lds_load16(yd[n % kKS] + SO + (n / kKS) * kHB); };
 #pragma unroll
     for (int n = 0; n < RA; ++n) {
-      rq[n] = rowq(n);
-      rd[n] = rowd(n);
+      rq[n] = nq[n];
+      rd[n] = nd[n];
     }
-    fence();
+    // Transpose reads of blocks C and D: rows 16u .. 16u + 15 of head j.
+    auto trd = [&](int j, int u, int d) {
+      const uint32_t o = SO + j * kHB + u * 16 * kRB;
+      return cat(lds_read_tr_at(td0[d] + o), lds_read_tr_at(td1[d] + o));
+    };
+    auto trq = [&](int j, int u, int d) {
+      const uint32_t o = SO + j * kHB + u * 16 * kRB;
+      return cat(lds_read_tr_at(tq0[d] + o), lds_read_tr_at(tq1[d] + o));
+    };
+    // product m of a head: m < 8 -> dV (u = m / 4, d = m % 4), else dK
+    auto opnd = [&](int j, int m) { return m < 8 ? trd(j, m / 4, m % 4) : trq(j, (m - 8) / 4, (m - 8) % 4); };
+    bf16x8 tf[TA + 1];
     bf16x8 pb[NH][2], dsb[NH][2];
     float pm[NH][2] = {{0.f, 0.f}, {0.f, 0.f}};  // ADAPT: largest P per head and 16-row half
     Cursor c4;
@@ -440,6 +454,8 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
       if (n + RA < 2 * kKS) {
         rq[(n + RA) % (RA + 1)] = rowq(n + RA);
         rd[(n + RA) % (RA + 1)] = rowd(n + RA);
+      } else if (n >= 2 * kKS - TA) {
+        tf[n - (2 * kKS - TA)] = opnd(0, n - (2 * kKS - TA));  // block C's first operands
       }
       const int j = n / kKS, k = n % kKS;
       sa[j] = mfma32(rq[n % (RA + 1)], kf[k], sa[j]);
@@ -477,16 +493,6 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
     // ---- C and D: dV^T += dO_j^T P_j, dK^T += Q_j^T dS_j (queries are the
     // contraction index), head 0 under the softmax of head 1, head 1 under
     // dS_1 and the next step's starts.  Per product: two transpose reads.
-    auto trd = [&](int j, int u, int d) {
-      const uint32_t o = SO + j * kHB + u * 16 * kRB;
-      return cat(lds_read_tr_at(td0[d] + o), lds_read_tr_at(td1[d] + o));
-    };
-    auto trq = [&](int j, int u, int d) {
-      const uint32_t o = SO + j * kHB + u * 16 * kRB;
-      return cat(lds_read_tr_at(tq0[d] + o), lds_read_tr_at(tq1[d] + o));
-    };
-    // product m of a head: m < 8 -> dV (u = m / 4, d = m % 4), else dK
-    auto opnd = [&](int j, int m) { return m < 8 ? trd(j, m / 4, m % 4) : trq(j, (m - 8) / 4, (m - 8) % 4); };
     // ADAPT: the 16-row half u of head j also carries P - bf16(P) and
     // dS - bf16(dS) (from P_j and dS_j, still in sa[j], da[j]) as second bf16
     // terms when some probability of that half reaches hilo_tau: 4 dV and 4 dK
@@ -513,10 +519,6 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
       second_terms(0);
       fence();
     }
-    bf16x8 tf[TA + 1];
-#pragma unroll
-    for (int n = 0; n < TA; ++n) tf[n] = opnd(0, n);
-    fence();
 #pragma unroll
     for (int n = 0; n < 32; ++n) {
       if (n + TA < 32) tf[(n + TA) % (TA + 1)] = opnd((n + TA) / 16, (n + TA) % 16);
@@ -556,6 +558,11 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
       load_head_starts(NX, c1, 1, sa[1], da[1]);
       fence();
     }
+#pragma unroll
+    for (int i = 0; i < RA; ++i) {
+      nq[i] = lds_load16(yq[i] + NX * kTileB);
+      nd[i] = lds_load16(yd[i] + NX * kTileB);
+    }
     asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(kIPW + 1) : "memory");
     c0 = c1;
     c1 = c2;
@@ -579,6 +586,11 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
   copy_step(2, c2);
   asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(kIPW + 1) : "memory");  // steps 0 and 1 landed
   load_starts(0, c0);
+#pragma unroll
+  for (int i = 0; i < RA; ++i) {
+    nq[i] = lds_load16(yq[i]);
+    nd[i] = lds_load16(yd[i]);
+  }
   using I0 = std::integral_constant<int, 0>;
   using I1 = std::integral_constant<int, 1>;
   using I2 = std::integral_constant<int, 2>;
