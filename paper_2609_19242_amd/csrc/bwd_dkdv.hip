@@ -418,7 +418,7 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
   // One step on stage ST: the copies of step `cp` into stage CP go out under
   // its first products, the starts of step `nx` (stage NX) are loaded under its
   // last ones, and the walk advances under the softmax of head 0.
-  constexpr int TA = 4;  // transpose-read pairs in flight ahead of the dV/dK products
+  constexpr int TA = 8;  // transpose-read pairs in flight ahead of the dV/dK products
   Cursor c0, c1, c2, c3;
   CopyPlan cpl;  // copies of step c3, planned during the step before
   auto run_step = [&](auto st_c, auto nx_c, int cp_stage) __attribute__((always_inline)) {
@@ -454,9 +454,8 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
       if (n + RA < 2 * kKS) {
         rq[(n + RA) % (RA + 1)] = rowq(n + RA);
         rd[(n + RA) % (RA + 1)] = rowd(n + RA);
-      } else if (n >= 2 * kKS - TA) {
-        tf[n - (2 * kKS - TA)] = opnd(0, n - (2 * kKS - TA));  // block C's first operands
       }
+      if (n >= 2 * kKS - TA) tf[n - (2 * kKS - TA)] = opnd(0, n - (2 * kKS - TA));  // block C's first operands
       const int j = n / kKS, k = n % kKS;
       sa[j] = mfma32(rq[n % (RA + 1)], kf[k], sa[j]);
       da[j] = mfma32(rd[n % (RA + 1)], vf[k], da[j]);

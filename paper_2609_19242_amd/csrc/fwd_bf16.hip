@@ -210,6 +210,22 @@ __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
           }
       }
 
+      // V^T operands of P V (V tile by transpose reads), product n = (16-key
+      // step n / DT, d tile n % DT).  The first PA are read here, before the
+      // softmax, whose vector work then covers their latency; the rest are
+      // read PA products ahead.
+      const uint32_t zt0 = sb + TB + ytr0, zt1 = sb + TB + ytr1;
+      auto vop = [&](int n) {
+        const int u = n / DT, d = n % DT;
+        return cat(lds_read_tr_at((zt0 ^ (64u * d)) + u * 16 * RB), lds_read_tr_at((zt1 ^ (64u * d)) + u * 16 * RB));
+      };
+      constexpr int PA = 4, NP = 4 * DT;
+      bf16x8 vr[PA + 1];
+      if constexpr (HM != 1) {
+#pragma unroll
+        for (int n = 0; n < PA; ++n) vr[n] = vop(n);
+      }
+
       // HM 2: a 16-key chunk of the tile also carries P - bf16(P) as a second
       // bf16 term when some lane's largest p in it reaches hilo_tau times the
       // lane's running sum.  The row sum only grows, so an element whose final
@@ -267,16 +283,13 @@ __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
 
       // O^T[d][q] += sum_key V[key][d] P[q][key]; the key order inside each
       // 16-key step follows the S^T register layout (see device.hpp).
-      const uint32_t zt0 = sb + TB + ytr0, zt1 = sb + TB + ytr1;  // V tile by transpose reads
       auto pv = [&](const bf16x8 (&pp)[4]) __attribute__((always_inline)) {
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-#pragma unroll
-          for (int d = 0; d < DT; ++d) {
-            const bf16x8 va = cat(lds_read_tr_at((zt0 ^ (64u * d)) + u * 16 * RB),
-                                  lds_read_tr_at((zt1 ^ (64u * d)) + u * 16 * RB));
-            acc[d] = mfma32(va, pp[u], acc[d]);
-          }
+        for (int n = 0; n < NP; ++n) {
+          if (n + PA < NP) vr[(n + PA) % (PA + 1)] = vop(n + PA);
+          acc[n % DT] = mfma32(vr[n % (PA + 1)], pp[n / DT], acc[n % DT]);
+          __builtin_amdgcn_sched_barrier(0);
         }
       };
       if constexpr (HM == 1) {
