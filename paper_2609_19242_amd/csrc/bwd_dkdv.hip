@@ -103,6 +103,45 @@ __device__ __forceinline__ f32x4 lds_f4(uint32_t a) {
   return *(__attribute__((address_space(3))) const f32x4*)(uintptr_t)a;
 }
 
+// Descriptors of step i of a key tile's walk (walk_step): its 32-row block,
+// q | partial << 1, and words 0-2 of the buffer resources of its tensor rows
+// (32 rows x 2 heads from block s of range q, head pair hp) and of its
+// statistics row; steps past the end copy nothing and are not partial.  Plain
+// scalar parameters: as a lambda over captured variables, the compiler turned
+// the per-lane selects into indexed loads from a stack copy of the captures.
+struct StepDesc {
+  int s, flags;
+  uint32_t t0, t1, t2, l0, l1, l2;
+};
+__device__ __forceinline__ StepDesc step_desc(const WalkPlan& wp, int i, int64_t H, bool stats_wave, int len_0,
+                                              int len_1, int f0_0, int f0_1, int f1_0, int f1_1, uint32_t lrec_0,
+                                              uint32_t lrec_1, uint64_t tb_0, uint64_t tb_1, uint64_t lb_0,
+                                              uint64_t lb_1) {
+  constexpr int BM = kBM, NH = kNH;
+  const WalkStep ws = walk_step(wp, i);
+  const bool live = ws.live;
+  const int q = live ? ws.q : 0;
+  const int blk = ws.s;
+  const int row0 = live ? blk * BM : 0;
+  const int len = q ? len_1 : len_0;
+  const int nrows = imin(BM, len - row0);
+  const int hoff = ws.hp * NH;
+  StepDesc d;
+  d.s = blk;
+  const bool part = live && !(blk >= (q ? f0_1 : f0_0) && blk < (q ? f1_1 : f1_0));
+  d.flags = q | (part ? 2 : 0);
+  const uint64_t tp = (q ? tb_1 : tb_0) + (uint64_t)(((int64_t)row0 * H + hoff) * kD * 2);
+  d.t0 = (uint32_t)tp;
+  d.t1 = (uint32_t)(tp >> 32) & 0xffffu;
+  d.t2 = live ? (uint32_t)((nrows - 1) * (int)H + NH) * kD * 2 : 0u;
+  const int loff = live ? hoff * len + row0 : 0;
+  const uint64_t lp = (q ? lb_1 : lb_0) + (uint64_t)loff * 4u;
+  d.l0 = (uint32_t)lp;
+  d.l1 = (uint32_t)(lp >> 32) & 0xffffu;
+  d.l2 = (live && stats_wave) ? (q ? lrec_1 : lrec_0) - (uint32_t)loff * 4u : 0u;
+  return d;
+}
+
 // ADAPT: a step also carries P - bf16(P) and dS - bf16(dS) of a head's
 // 16-row half as second bf16 terms when some probability of that half reaches
 // hilo_tau (8 more products: head 0's after block B, head 1's after block D,
@@ -183,7 +222,7 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
     const float* lb;
     uint32_t lrec;
   };
-  auto make_span = [&](int q) -> Span {
+  auto make_span = [&](int q) __attribute__((always_inline)) -> Span {
     Span sp{0, 0, 0, 0, 0, 0, 0, 0, nullptr, nullptr, 0u};
     if (q >= a.n_q) return sp;
     const QRangeArg& qr = a.qr[q];
@@ -218,29 +257,9 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
   const Span R0 = make_span(0), R1 = make_span(1);
   auto sel2 = [](int q, auto v0, auto v1) { return q ? v1 : v0; };
 #define BDLM_PICK(f, q) sel2((q), R0.f, R1.f)
-  auto active = [](const Span& sp, int s) { return sp.s0 <= s && s < sp.s1; };
-  auto below = [](const Span& sp, int s) {
-    const int cand = imin(s - 1, sp.s1 - 1);
-    return cand >= sp.s0 ? cand : -1;
-  };
-  struct Cursor {
-    int q, hp, s;
-  };
-  const int npairs = a.group / NH;
-  // Next (range, head pair, step) of the walk, as selects only (no branches,
-  // so the compiler can place it between the products of a step).
-  auto advance = [&](Cursor c) __attribute__((always_inline)) -> Cursor {
-    const bool live = c.s >= 0;
-    const bool wrap = c.hp + 1 >= npairs;
-    const bool next_range = c.q == 0 && active(R1, c.s);  // the other range at the same step
-    const int s_next = imax(below(R0, c.s), below(R1, c.s));
-    const int q_first = active(R0, s_next) ? 0 : 1;
-    Cursor n;
-    n.hp = wrap ? 0 : c.hp + 1;
-    n.q = !wrap ? c.q : next_range ? 1 : (s_next >= 0 ? q_first : 0);
-    n.s = (!wrap || next_range) ? c.s : s_next;
-    return live ? n : c;
-  };
+  // The walk by step index (walk_plan, walk_step).
+  const WalkPlan wp = walk_plan(R0.s0, R0.s1, R1.s0, R1.s1, a.group / NH);
+  const int nsteps = wp.nsteps;
 
   // ---- copies.  Instruction i of a wave is instruction (w & 1) * kIPW + i of
   // its tensor; the per-lane global offsets are constant over the walk.
@@ -261,21 +280,38 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
     u32x4 rt, rl;   // resources: the wave's tensor rows, its -LSE/scale or -D row
     uint32_t lvo;   // per-lane offset of the dword copy
   };
-  // The copy resources of step c (selects only).
-  auto copy_plan = [&](const Cursor c) __attribute__((always_inline)) -> CopyPlan {
-    const bool live = c.s >= 0;
-    const int q = live ? c.q : 0;
-    const int row0 = live ? c.s * BM : 0;
-    const int len = BDLM_PICK(len, q);
-    const int nrows = imin(BM, len - row0);
-    const int hoff = c.hp * NH;
-    const uint32_t bytes = live ? (uint32_t)((nrows - 1) * (int)H + NH) * kD * 2 : 0u;
+  // Step descriptors, 64 steps at a time: lane l of a batch holds step
+  // base + l (step_desc); a step reads them back with one readlane each.
+  // Steps past the walk's end copy nothing (zero-size resources) and are not
+  // partial.
+  const int len_0 = R0.len, len_1 = R1.len, f0_0 = R0.f0, f0_1 = R1.f0, f1_0 = R0.f1, f1_1 = R1.f1;
+  const uint32_t lrec_0 = R0.lrec, lrec_1 = R1.lrec;
+  const uint64_t tb_0 = (uint64_t)(uintptr_t)R0.tb, tb_1 = (uint64_t)(uintptr_t)R1.tb;
+  const uint64_t lb_0 = (uint64_t)(uintptr_t)R0.lb, lb_1 = (uint64_t)(uintptr_t)R1.lb;
+  auto make_batch = [&](int base) __attribute__((always_inline)) -> StepDesc {
+    return step_desc(wp, base + lane, H, w >= 2, len_0, len_1, f0_0, f0_1, f1_0, f1_1, lrec_0, lrec_1, tb_0, tb_1,
+                     lb_0, lb_1);
+  };
+  StepDesc bt;
+  int bbase = 0;
+  // Per-lane offsets of the dword copy for each range (rows of two heads).
+  const uint32_t lvo0 = (uint32_t)(((lane >> 5) * R0.len + (lane & 31)) * 4);
+  const uint32_t lvo1 = (uint32_t)(((lane >> 5) * R1.len + (lane & 31)) * 4);
+  auto rl = [&](uint32_t v, int i) __attribute__((always_inline)) {
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, i - bbase);
+  };
+  // The copy resources of step i.
+  auto copy_plan = [&](int i) __attribute__((always_inline)) -> CopyPlan {
     CopyPlan cp;
-    cp.rt = rsrc_words(BDLM_PICK(tb, q) + ((int64_t)row0 * H + hoff) * kD, bytes);
-    const int loff = hoff * len + row0;
-    const uint32_t lbytes = (live && w >= 2) ? BDLM_PICK(lrec, q) - (uint32_t)loff * 4u : 0u;
-    cp.rl = rsrc_words(BDLM_PICK(lb, q) + loff, lbytes);
-    cp.lvo = (uint32_t)(((lane >> 5) * len + (lane & 31)) * 4);
+    cp.rt[0] = rl(bt.t0, i);
+    cp.rt[1] = rl(bt.t1, i);
+    cp.rt[2] = rl(bt.t2, i);
+    cp.rt[3] = 0x00020000u;
+    cp.rl[0] = rl(bt.l0, i);
+    cp.rl[1] = rl(bt.l1, i);
+    cp.rl[2] = rl(bt.l2, i);
+    cp.rl[3] = 0x00020000u;
+    cp.lvo = (rl((uint32_t)bt.flags, i) & 1) ? lvo1 : lvo0;
     return cp;
   };
   auto copy_issue = [&](const CopyPlan& cp, int st, int i) __attribute__((always_inline)) {
@@ -287,18 +323,18 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
       dma4(cp.rl, ldst, cp.lvo);
     }
   };
-  auto copy_step = [&](int st, const Cursor c) __attribute__((always_inline)) {
-    const CopyPlan cp = copy_plan(c);
+  // The resource words come from readlane, a vector instruction writing scalar
+  // registers; a buffer access reading them needs five wait states after it,
+  // which the compiler does not insert before inline assembly.  Every plan
+  // therefore passes an s_nop 4 that takes its words as inputs before its copies.
+  auto plan_ready = [](const CopyPlan& cp) __attribute__((always_inline)) {
+    asm volatile("s_nop 4" ::"s"(cp.rt), "s"(cp.rl), "v"(cp.lvo));
+  };
+  auto copy_step = [&](int st, int i) __attribute__((always_inline)) {
+    const CopyPlan cp = copy_plan(i);
+    plan_ready(cp);
 #pragma unroll
     for (int i = 0; i <= kIPW; ++i) copy_issue(cp, st, i);
-  };
-  // Pins scalar walk values at a point of the step's instruction order: an
-  // empty asm statement the values pass through (in) or must exist at (use).
-  auto pin_in = [](Cursor& c) __attribute__((always_inline)) {
-    asm volatile("" : "+s"(c.s), "+s"(c.q), "+s"(c.hp));
-  };
-  auto pin_use = [](const Cursor& c) __attribute__((always_inline)) {
-    asm volatile("" ::"s"(c.s), "s"(c.q), "s"(c.hp));
   };
 
   const float c = a.scale_log2;
@@ -334,8 +370,8 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
   // (its stage is complete from the barrier before that step on).
   constexpr int RA = 4;  // row-read pairs in flight ahead of the score products
   bf16x8 nq[RA], nd[RA];
-  // Load the starts of step `cu` (stage st) and apply the mask of partly visible steps.
-  auto load_starts = [&](int st, const Cursor cu) __attribute__((always_inline)) {
+  // Load the starts of step i (stage st) and apply the mask of partly visible steps.
+  auto load_starts = [&](int st, int si) __attribute__((always_inline)) {
     const uint32_t base = ystat + st * kStatB;
 #pragma unroll
     for (int j = 0; j < NH; ++j)
@@ -349,14 +385,12 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
           da[j][4 * g4 + e] = dd[e];
         }
       }
-    const int q = cu.s >= 0 ? cu.q : 0;
+    const int fl = (int)rl((uint32_t)bt.flags, si), q = fl & 1;
     // Partly visible steps: hidden scores start at -inf.  The compare and the
     // selects are inline assembly inside a wave-uniform branch: as plain code
     // the compiler speculates them onto every step.
-    const int partial =
-        __builtin_amdgcn_readfirstlane((cu.s >= BDLM_PICK(f0, q) && cu.s < BDLM_PICK(f1, q)) ? 0 : 1);
-    if (partial) {
-      const int mbase = BDLM_PICK(pos0, q) + cu.s * BM + 4 * half - BDLM_PICK(qa, q);
+    if (fl & 2) {
+      const int mbase = BDLM_PICK(pos0, q) + (int)rl((uint32_t)bt.s, si) * BM + 4 * half - BDLM_PICK(qa, q);
       const int lane_qw = BDLM_PICK(qw, q);
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
@@ -380,7 +414,7 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
 
   // The starts of head j of step `cu` (stage st) into s, d, with the mask of
   // partly visible steps (the values load_starts gives that head).
-  auto load_head_starts = [&](int st, const Cursor cu, int j, f32x16& s, f32x16& d) __attribute__((always_inline)) {
+  auto load_head_starts = [&](int st, int si, int j, f32x16& s, f32x16& d) __attribute__((always_inline)) {
     const uint32_t base = ystat + st * kStatB;
 #pragma unroll
     for (int g4 = 0; g4 < 4; ++g4) {
@@ -392,11 +426,9 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
         d[4 * g4 + e] = dd[e];
       }
     }
-    const int q = cu.s >= 0 ? cu.q : 0;
-    const int partial =
-        __builtin_amdgcn_readfirstlane((cu.s >= BDLM_PICK(f0, q) && cu.s < BDLM_PICK(f1, q)) ? 0 : 1);
-    if (partial) {
-      const int mbase = BDLM_PICK(pos0, q) + cu.s * BM + 4 * half - BDLM_PICK(qa, q);
+    const int fl = (int)rl((uint32_t)bt.flags, si), q = fl & 1;
+    if (fl & 2) {
+      const int mbase = BDLM_PICK(pos0, q) + (int)rl((uint32_t)bt.s, si) * BM + 4 * half - BDLM_PICK(qa, q);
       const int lane_qw = BDLM_PICK(qw, q);
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
@@ -419,8 +451,8 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
   // its first products, the starts of step `nx` (stage NX) are loaded under its
   // last ones, and the walk advances under the softmax of head 0.
   constexpr int TA = 8;  // transpose-read pairs in flight ahead of the dV/dK products
-  Cursor c0, c1, c2, c3;
-  CopyPlan cpl;  // copies of step c3, planned during the step before
+  int i0 = 0;    // the current step
+  CopyPlan cpl;  // copies of step i0 + 3, planned during the step before
   auto run_step = [&](auto st_c, auto nx_c, int cp_stage) __attribute__((always_inline)) {
     constexpr int ST = decltype(st_c)::value, NX = decltype(nx_c)::value;
     constexpr uint32_t SO = ST * kTileB;  // stage offset inside a tensor region
@@ -448,7 +480,6 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
     bf16x8 tf[TA + 1];
     bf16x8 pb[NH][2], dsb[NH][2];
     float pm[NH][2] = {{0.f, 0.f}, {0.f, 0.f}};  // ADAPT: largest P per head and 16-row half
-    Cursor c4;
 #pragma unroll
     for (int n = 0; n < 2 * kKS; ++n) {
       if (n + RA < 2 * kKS) {
@@ -460,13 +491,8 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
       sa[j] = mfma32(rq[n % (RA + 1)], kf[k], sa[j]);
       da[j] = mfma32(rd[n % (RA + 1)], vf[k], da[j]);
       if (n <= kIPW) copy_issue(cpl, cp_stage, n);
-      if (n == kIPW + 1) {
-        pin_in(c3);
-        c4 = advance(c3);
-      }
-      if (n == kIPW + 2) pin_use(c4);
-      if (n == kIPW + 3) cpl = copy_plan(c4);
-      if (n == kIPW + 4) asm volatile("" ::"s"(cpl.rt), "s"(cpl.rl), "v"(cpl.lvo));
+      if (n == kIPW + 3) cpl = copy_plan(i0 + 4);
+      if (n == kIPW + 4) plan_ready(cpl);
 
       if (j == 1) {
         // softmax of head 0: two scores per product pair
@@ -545,8 +571,8 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
           for (int e = 0; e < 4; ++e) dsb[1][(i0 + e) >> 3][(i0 + e) & 7] = to_bf16(da[1][i0 + e]);
         }
       } else if (m == 8) {
-        if constexpr (!ADAPT) load_starts(NX, c1);
-        else load_head_starts(NX, c1, 0, sa[0], da[0]);
+        if constexpr (!ADAPT) load_starts(NX, i0 + 1);
+        else load_head_starts(NX, i0 + 1, 0, sa[0], da[0]);
       }
       fence();
     }
@@ -554,7 +580,7 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
       // head 1's second terms need P_1 and dS_1, which its next starts
       // overwrite: both come after the products here
       second_terms(1);
-      load_head_starts(NX, c1, 1, sa[1], da[1]);
+      load_head_starts(NX, i0 + 1, 1, sa[1], da[1]);
       fence();
     }
 #pragma unroll
@@ -563,28 +589,23 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
       nd[i] = lds_load16(yd[i] + NX * kTileB);
     }
     asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(kIPW + 1) : "memory");
-    c0 = c1;
-    c1 = c2;
-    c2 = c3;
-    c3 = c4;
+    ++i0;
   };
 
   // ---- the walk: four LDS stages, copies three steps ahead.  At the barrier
   // closing step i every wave has waited for its copies of step i + 2 (only
   // those of step i + 3 stay in flight) and has finished reading stage i,
   // which the copies issued next overwrite.
-  c0.s = imax(below(R0, kBig), below(R1, kBig));
-  c0.q = (c0.s >= 0 && !active(R0, c0.s)) ? 1 : 0;
-  c0.hp = 0;
-  c1 = advance(c0);
-  c2 = advance(c1);
-  c3 = advance(c2);
-  cpl = copy_plan(c3);
-  copy_step(0, c0);
-  copy_step(1, c1);
-  copy_step(2, c2);
+  // A batch covers steps bbase .. bbase + 63 and is renewed every 56 steps: an
+  // iteration of the loop below starting at step i0 reads steps up to i0 + 7.
+  bt = make_batch(0);
+  cpl = copy_plan(3);
+  plan_ready(cpl);
+  copy_step(0, 0);
+  copy_step(1, 1);
+  copy_step(2, 2);
   asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(kIPW + 1) : "memory");  // steps 0 and 1 landed
-  load_starts(0, c0);
+  load_starts(0, 0);
 #pragma unroll
   for (int i = 0; i < RA; ++i) {
     nq[i] = lds_load16(yq[i]);
@@ -594,13 +615,17 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
   using I1 = std::integral_constant<int, 1>;
   using I2 = std::integral_constant<int, 2>;
   using I3 = std::integral_constant<int, 3>;
-  while (c0.s >= 0) {
+  while (i0 < nsteps) {
+    if (i0 - bbase >= 56) {
+      bbase = i0;
+      bt = make_batch(bbase);
+    }
     run_step(I0{}, I1{}, 3);
-    if (c0.s < 0) break;
+    if (i0 >= nsteps) break;
     run_step(I1{}, I2{}, 0);
-    if (c0.s < 0) break;
+    if (i0 >= nsteps) break;
     run_step(I2{}, I3{}, 1);
-    if (c0.s < 0) break;
+    if (i0 >= nsteps) break;
     run_step(I3{}, I0{}, 2);
   }
   // Copies still in flight target stages nobody reads; they must land before

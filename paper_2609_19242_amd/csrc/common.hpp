@@ -200,6 +200,71 @@ hipError_t launch_bwd_dkdv(const AttnArgs& a, hipStream_t s);
 hipError_t launch_bwd_dq_bf16(const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_bwd_f32(const AttnArgs& a, int head_dim, hipStream_t s);
 
+// The walk of a key tile of the scheduled dK/dV kernel over its visible query
+// rows, by step index.  The rows come as up to two query ranges; range r is
+// seen by the tile's keys in the 32-row blocks [a_r, b_r) (a_r = b_r = 0 when
+// empty).  Step i is (range q, block s, head pair hp): blocks from the top
+// down, at each block every range active there (range 0 first), each with its
+// npairs head pairs in order.  The block axis splits at the four range ends
+// into at most three segments with a fixed set of active ranges: segment k
+// covers blocks [p_{k+1}, p_k) with cnt_k active ranges (the first q0_k), so
+// step i follows from its segment in closed form.
+struct WalkPlan {
+  int p0, p1, p2, p3;  // range ends, descending
+  int st1, st2, nsteps;  // first steps of segments 1 and 2; steps in all
+  int cnt0, cnt1, cnt2, q00, q01, q02, npairs;
+};
+__host__ __device__ inline WalkPlan walk_plan(int a0, int b0, int a1, int b1, int npairs) {
+  WalkPlan w;
+  int p0 = b0, p1 = a0, p2 = b1, p3 = a1;
+  auto cx = [](int& x, int& y) {
+    const int hi = imax(x, y), lo = imin(x, y);
+    x = hi;
+    y = lo;
+  };
+  cx(p0, p1);
+  cx(p2, p3);
+  cx(p0, p2);
+  cx(p1, p3);
+  cx(p1, p2);
+  auto act = [](int a, int b, int blk) { return a <= blk && blk < b ? 1 : 0; };
+  w.p0 = p0;
+  w.p1 = p1;
+  w.p2 = p2;
+  w.p3 = p3;
+  w.cnt0 = act(a0, b0, p1) + act(a1, b1, p1);
+  w.cnt1 = act(a0, b0, p2) + act(a1, b1, p2);
+  w.cnt2 = act(a0, b0, p3) + act(a1, b1, p3);
+  w.q00 = act(a0, b0, p1) ? 0 : 1;
+  w.q01 = act(a0, b0, p2) ? 0 : 1;
+  w.q02 = act(a0, b0, p3) ? 0 : 1;
+  w.npairs = npairs;
+  w.st1 = (p0 - p1) * w.cnt0 * npairs;
+  w.st2 = w.st1 + (p1 - p2) * w.cnt1 * npairs;
+  w.nsteps = w.st2 + (p2 - p3) * w.cnt2 * npairs;
+  return w;
+}
+struct WalkStep {
+  int q, s, hp;
+  bool live;  // i < nsteps (q, s, hp are meaningless otherwise)
+};
+__host__ __device__ inline WalkStep walk_step(const WalkPlan& w, int i) {
+  const bool k1 = i >= w.st1, k2 = i >= w.st2;
+  const int top = (k2 ? w.p2 : k1 ? w.p1 : w.p0) - 1;
+  const int cnt = k2 ? w.cnt2 : k1 ? w.cnt1 : w.cnt0;
+  const int q0 = k2 ? w.q02 : k1 ? w.q01 : w.q00;
+  const int off = i - (k2 ? w.st2 : k1 ? w.st1 : 0);
+  const int per = imax(cnt * w.npairs, 1);
+  const int sr = off / per, rem = off - sr * per;
+  const int ridx = rem >= w.npairs ? 1 : 0;
+  WalkStep st;
+  st.live = i >= 0 && i < w.nsteps;
+  st.hp = rem - ridx * w.npairs;
+  st.q = cnt == 2 ? ridx : q0;
+  st.s = top - sr;
+  return st;
+}
+
 // The dK/dV kernel of bwd_dkdv.hip (head_dim 128, single-term or adaptive
 // two-term dK/dV products, an even GQA group, at most two query ranges with
 // rows) starts its score and dP accumulators at -LSE/scale and -D, so the backward
