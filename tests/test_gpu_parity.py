@@ -347,6 +347,52 @@ def test_multi_range_fwd_bwd(split, heads):
     assert_close(f"{split} dV", torch.cat([t.cpu() for t in dvd], dim=1), dV, torch.bfloat16)
 
 
+@pytest.mark.parametrize("layout", ["gap", "gap-reversed", "offset"])
+def test_two_query_ranges_with_apart_spans(layout):
+    """Two query ranges whose visible 32-row blocks for a key tile do not nest:
+    for the clean key tile at 128 the spans are blocks [0, 2) and [4, 10) with a
+    gap between them, in either range order, and in "offset" [2, 4) and [5, 7).
+    Head_dim 128, bf16, an even GQA group and two query ranges: the backward runs
+    the scheduled dK/dV kernel, whose walk over such spans has its own segments
+    (walk_plan); checked against the oracle over the same ranges."""
+    Hq, Hkv, D = 8, 2, 128
+    L, M = 300, 12
+    q, k, v, do = joint_inputs(L, Hq, Hkv, D, torch.bfloat16, seed=77)
+    qrs = {"gap": [(CLEAN, 120, 60), (CORRUPTED, 0, 300)],
+           "gap-reversed": [(CORRUPTED, 0, 300), (CLEAN, 120, 60)],
+           "offset": [(CLEAN, 180, 120), (CORRUPTED, 100, 200)]}[layout]
+    krs = [(CLEAN, 0, 300), (CORRUPTED, 0, 300)]
+
+    def rows(t, rs):  # joint tensors hold corrupted rows [0, L) then clean rows [L, 2L)
+        return [t[:, (L if s == CLEAN else 0) + p0:(L if s == CLEAN else 0) + p0 + n].contiguous() for s, p0, n in rs]
+
+    qs, dos = rows(q, qrs), rows(do, qrs)
+    ks, vs = rows(k, krs), rows(v, krs)
+    p = bd.make_problem(1, L, M, Hq, Hkv, D, torch.bfloat16, out_f32=True)
+    QR = [Range(*r) for r in qrs]
+    KR = [Range(*r) for r in krs]
+    qd, dod = [t.to(DEV) for t in qs], [t.to(DEV) for t in dos]
+    kd, vd = [t.to(DEV) for t in ks], [t.to(DEV) for t in vs]
+    od = [torch.empty(t.shape, dtype=torch.float32, device=DEV) for t in qd]
+    ld = [torch.empty((1, Hq, t.shape[1]), dtype=torch.float32, device=DEV) for t in qd]
+    bd.attn_fwd(p, QR, qd, od, ld, KR, kd, vd)
+    dqd = [torch.empty(t.shape, dtype=torch.float32, device=DEV) for t in qd]
+    dkd = [torch.empty(t.shape, dtype=torch.float32, device=DEV) for t in kd]
+    dvd = [torch.empty(t.shape, dtype=torch.float32, device=DEV) for t in vd]
+    ws = torch.empty(bd.attn_bwd_workspace_bytes(p, QR), dtype=torch.uint8, device=DEV)
+    bd.attn_bwd(p, QR, qd, od, ld, dod, dqd, KR, kd, vd, dkd, dvd, ws)
+    torch.cuda.synchronize()
+
+    qall, doall = torch.cat(qs, dim=1), torch.cat(dos, dim=1)
+    kall, vall = torch.cat(ks, dim=1), torch.cat(vs, dim=1)
+    O, LSE = oracle.fwd(qall, kall, vall, qrs, krs, M)
+    dQ, dK, dV = oracle.bwd(qall, kall, vall, O, LSE, doall, qrs, krs, M)
+    assert_close(f"{layout} O", torch.cat([t.cpu() for t in od], dim=1), O, torch.bfloat16)
+    assert_close(f"{layout} dQ", torch.cat([t.cpu() for t in dqd], dim=1), dQ, torch.bfloat16)
+    assert_close(f"{layout} dK", torch.cat([t.cpu() for t in dkd], dim=1), dK, torch.bfloat16)
+    assert_close(f"{layout} dV", torch.cat([t.cpu() for t in dvd], dim=1), dV, torch.bfloat16)
+
+
 # ---------------------------------------------------------- degenerate calls
 def test_degenerate_ranges():
     """Zero-length query and key ranges next to ordinary ones change nothing
