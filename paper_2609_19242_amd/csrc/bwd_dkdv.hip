@@ -18,15 +18,19 @@
 // is written as four blocks of 16 matrix products each, with the vector and
 // scalar work placed under them and the order fixed by scheduling fences:
 //   A: S_0 = Q_0 K^T, dP_0 = dO_0 V^T (head 0)  under  the LDS-DMA copies of
-//      the step three ahead, the walk's next position and its copy plan
-//   B: S_1, dP_1 (head 1)      under  P_0 = exp2(c S_0), dS_0 = P_0 dP_0
+//      the step three ahead and the copy plan of the step after
+//   B: S_1, dP_1 (head 1)      under  P_0 = exp2(c S_0), dS_0 = P_0 dP_0, and
+//      the first operand reads of C
 //   C: dV += dO_0^T P_0, dK += Q_0^T dS_0   under  P_1 = exp2(c S_1)
-//   D: dV += dO_1^T P_1, dK += Q_1^T dS_1   under  dS_1 = P_1 dP_1, and the
-//      next step's accumulator starts
-// Every product's LDS operand is read four products ahead.  The walk is
-// branch-free, and empty asm statements pin its scalar work to its place in
-// the order (the compiler would otherwise hoist it to the top of the step,
-// where nothing overlaps it).
+//   D: dV += dO_1^T P_1, dK += Q_1^T dS_1   under  dS_1 = P_1 dP_1, the next
+//      step's accumulator starts, and its first row reads (issued before the
+//      step's barrier: that stage is complete from the barrier before)
+// Row operands are read four products ahead, transpose operands eight.  The
+// walk's bookkeeping is vector work: the descriptors of 64 steps (block,
+// range, partial flag, copy resource words) sit in the lanes of a few VGPRs,
+// computed every 56 steps from a closed form (walk_plan, walk_step), and a
+// step reads its own with readlane, so a step issues about 27 scalar
+// instructions where a scalar cursor took over a hundred.
 // S and dP accumulate on top of -LSE/scale and -D read from LDS (the dQ
 // kernel, which runs first, writes that form), so the softmax is one multiply
 // and one exp2 per score and dS one multiply; rows the mask hides start at
