@@ -4,6 +4,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -189,6 +190,17 @@ int64_t tile_ranges(R* rr, int n, int rows) {
   return tot;
 }
 
+// Query rows per bf16 forward / dQ workgroup: the short tile when the longest
+// key range (with a sliding window: the window plus one block, as a row sees
+// no more clean keys than the window and no corrupted keys outside its own
+// block) is at most the kernel's short-walk limit.  A throughput choice only.
+int bf16_query_rows(const bdlm_problem* p, int n_k, const bdlm_range* k_ranges, int64_t short_walk) {
+  int64_t walk = 0;
+  for (int j = 0; j < n_k; ++j) walk = std::max<int64_t>(walk, k_ranges[j].len);
+  if (p->window > 0) walk = std::min<int64_t>(walk, p->window + p->block_size);
+  return walk <= short_walk ? kQRowsShortBf16 : kQRowsLongBf16;
+}
+
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 bdlm_status check_grid(int64_t tiles, int64_t mult) {
@@ -236,7 +248,7 @@ bdlm_status bdlm_attn_fwd(const bdlm_problem* p, int32_t n_q, const bdlm_range* 
     a.kr[j].k = k[j];
     a.kr[j].v = v[j];
   }
-  const int rows = p->dtype == BDLM_BF16 ? kFwdRowsBf16 : kFwdRowsF32;
+  const int rows = p->dtype == BDLM_BF16 ? bf16_query_rows(p, n_k, k_ranges, kFwdShortWalk) : kFwdRowsF32;
   const int64_t tiles = tile_ranges(a.qr, n_q, rows);
   if ((st = check_grid(tiles, (int64_t)p->heads * p->batch)) != BDLM_OK) return st;
   a.total_tiles = (int32_t)tiles;
@@ -244,7 +256,7 @@ bdlm_status bdlm_attn_fwd(const bdlm_problem* p, int32_t n_q, const bdlm_range* 
   for (int i = 1; i < n_q; ++i)
     if (a.qr[i].ntiles != a.qr[0].ntiles) a.interleave = 0;
   const hipError_t e = p->dtype == BDLM_BF16
-                           ? timed(kKFwdBf16, stream, [&] { return launch_fwd_bf16(a, p->head_dim, stream); })
+                           ? timed(kKFwdBf16, stream, [&] { return launch_fwd_bf16(a, p->head_dim, rows, stream); })
                            : timed(kKFwdF32, stream, [&] { return launch_fwd_f32(a, p->head_dim, stream); });
   if (e != hipSuccess) return hip_fail(e, "forward launch");
   return BDLM_OK;
@@ -419,10 +431,11 @@ bdlm_status attn_bwd_impl(const bdlm_problem* p, int32_t n_q, const bdlm_range* 
   const int64_t tiles = tile_ranges(a.kr, n_k, keys);
   if ((st = check_grid(tiles, (int64_t)p->kv_heads * p->batch)) != BDLM_OK) return st;
   a.total_tiles = (int32_t)tiles;
-  // The dQ kernel walks query tiles of the forward's height.
+  // The dQ kernel walks query tiles (of its own height).
   AttnArgs aq = a;
+  const int dq_rows = bf16_query_rows(p, n_k, k_ranges, kDqShortWalk);
   if (p->dtype == BDLM_BF16) {
-    const int64_t qt = tile_ranges(aq.qr, n_q, kFwdRowsBf16);
+    const int64_t qt = tile_ranges(aq.qr, n_q, dq_rows);
     if ((st = check_grid(qt, (int64_t)p->heads * p->batch)) != BDLM_OK) return st;
     aq.total_tiles = (int32_t)qt;
     aq.interleave = 1;
@@ -463,7 +476,7 @@ bdlm_status attn_bwd_impl(const bdlm_problem* p, int32_t n_q, const bdlm_range* 
     // The dQ kernel computes D = rowsum(dO * O) itself and leaves each row's
     // statistics in the workspace for the dK/dV kernel, so it runs first.
     for (int j = 0; j < n_k; ++j) aq.order[j] = a.order[j];
-    e = timed(kKBwdDq, stream, [&] { return launch_bwd_dq_bf16(aq, p->head_dim, stream); });
+    e = timed(kKBwdDq, stream, [&] { return launch_bwd_dq_bf16(aq, p->head_dim, dq_rows, stream); });
     if (e != hipSuccess) return hip_fail(e, "backward dQ launch");
     e = timed(kKBwdBf16, stream, [&] {
       if (!a.stats_form) return launch_bwd_bf16(a, p->head_dim, stream);

@@ -22,8 +22,9 @@ namespace {
 
 constexpr float kLog2e = 1.44269504088896340736f;
 
-template <int D, int NW, int HM>
-__global__ __launch_bounds__(NW * 64) void bwd_dq_kernel(const AttnArgs a) {
+template <int D, int NW, int NST, int HM>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2))) void bwd_dq_kernel(
+    const AttnArgs a) {
   constexpr int BM = NW * 32, BN = 64, KS = D / 16, DT = D / 32;
   // K and V tiles with swizzled rows: K serves both its row reads (S^T) and
   // its transpose reads (K^T), V its row reads (dP^T).
@@ -33,7 +34,7 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_kernel(const AttnArgs a) {
   // waves 0 .. NW/2 - 1 copy K and the others V, IPW instructions each.
   constexpr int TI = BN * D / 8 / 64, IPW = TI / (NW / 2);
   static_assert(TI % (NW / 2) == 0, "whole copy instructions per wave");
-  __shared__ __attribute__((aligned(256))) bf16 lds[3 * STAGE];
+  __shared__ __attribute__((aligned(256))) bf16 lds[NST * STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, half = lane >> 5;
@@ -131,7 +132,7 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_kernel(const AttnArgs a) {
     return c;
   };
   const int64_t HKV = a.kv_heads;
-  // The copy cursor runs two tiles ahead of the compute cursor and carries
+  // The copy cursor runs NST - 1 tiles ahead of the compute cursor and carries
   // the source pointer of its tile (this wave's tensor, batch and KV head
   // applied) and the rows left in its range, so that advancing inside a range
   // is one pointer increment; both are recomputed only when the range changes.
@@ -163,36 +164,47 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_kernel(const AttnArgs a) {
   // LDS-DMA copy of the cursor's tile into stage st (empty copies past the
   // last tile, so every wave issues IPW per tile); rows past the range end
   // read zeros.
-  uint32_t voff[IPW];
+  // One instruction covers 512 / D rows and the chunk swizzle repeats every
+  // 16 rows, so instructions PI = D / 32 apart share their lane offsets and
+  // read through a resource based 16 rows further on (its size cut by as much).
+  constexpr int PI = IPW < D / 32 ? IPW : D / 32, NB = IPW / PI;
+  static_assert(IPW % PI == 0, "whole offset periods per wave");
+  uint32_t voff[PI];
   const int cw = w % (NW / 2);
 #pragma unroll
-  for (int i = 0; i < IPW; ++i) voff[i] = swz_src_offset<D>((cw * IPW + i) * 64 + lane, HKV * D);
+  for (int i = 0; i < PI; ++i) voff[i] = swz_src_offset<D>((cw * IPW + i) * 64 + lane, HKV * D);
   const bf16* const any_src = (const bf16*)a.kr[0].k;
   auto copy_tile = [&](bf16* st, const CopyCur& cc) __attribute__((always_inline)) {
     const int nrows = cc.c.have ? imin(BN, cc.rows_left) : 0;
-    const uint32_t bytes = cc.c.have ? (uint32_t)(((nrows - 1) * (int)HKV * D + D) * 2) : 0u;
-    const auto r = make_rsrc(cc.c.have ? cc.src : any_src, bytes);
     bf16* dst = st + (kwave ? 0 : BN * D) + cw * IPW * 512;
 #pragma unroll
-    for (int i = 0; i < IPW; ++i) buf_to_lds<16>(r, dst + i * 512, voff[i], 0);
+    for (int k = 0; k < NB; ++k) {
+      const int nr = nrows - 16 * k;
+      const uint32_t bytes = nr > 0 ? (uint32_t)(((nr - 1) * (int)HKV * D + D) * 2) : 0u;
+      const auto r = make_rsrc(nr > 0 ? cc.src + (int64_t)16 * k * HKV * D : any_src, bytes);
+#pragma unroll
+      for (int i = 0; i < PI; ++i) buf_to_lds<16>(r, dst + (k * PI + i) * 512, voff[i], 0);
+    }
   };
   // Per-lane parts of the swizzled read addresses (device.hpp).
   const uint32_t yrow = swz_row_part<D>(l32, half);
   const uint32_t ytr0 = swz_tr_part<D>(G, sl, 0), ytr1 = swz_tr_part<D>(G, sl, 8);
 
-  // Three LDS stages, copies two tiles ahead (as in the forward).
+  // NST LDS stages, copies NST - 1 tiles ahead (as in the forward: 8 waves
+  // and three stages on long walks, 4 waves and two on short ones).
   KCur c0;
   c0.have = find_key_tile(a, 0, qr.stream, pq0, pq1, BN, c0.j, c0.t, c0.t1, c0.f0, c0.f1);
   CopyCur cp = copy_seek(CopyCur{c0, any_src, 0});
-  copy_tile(lds, cp);
-  cp = copy_next(cp);
-  copy_tile(lds + STAGE, cp);
-  cp = copy_next(cp);
-  vm_wait_barrier<IPW>();
+#pragma unroll
+  for (int s = 0; s < NST - 1; ++s) {
+    copy_tile(lds + s * STAGE, cp);
+    cp = copy_next(cp);
+  }
+  vm_wait_barrier<IPW * (NST - 2)>();
   int cur = 0;
   int lane_lo = 0, lane_w = 0, lane_j = -1;
   while (c0.have) {
-    copy_tile(lds + (cur == 0 ? 2 : cur - 1) * STAGE, cp);
+    copy_tile(lds + (cur == 0 ? NST - 1 : cur - 1) * STAGE, cp);
     const int j = c0.j, t = c0.t, f0 = c0.f0, f1 = c0.f1;
     if (lane_j != j) {
       lane_key_interval(a, j, qr.stream, pq, lane_lo, lane_w);
@@ -316,8 +328,8 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_kernel(const AttnArgs a) {
       }
     }
 
-    vm_wait_barrier<IPW>();
-    cur = cur == 2 ? 0 : cur + 1;
+    vm_wait_barrier<IPW * (NST - 2)>();
+    cur = cur == NST - 1 ? 0 : cur + 1;
     c0 = next_tile(c0);
     cp = copy_next(cp);
   }
@@ -355,23 +367,30 @@ __global__ __launch_bounds__(NW * 64) void bwd_dq_kernel(const AttnArgs a) {
 
 // HM of the kernel: 0 single-term P (dS), 1 two-term on every tile, 2
 // two-term on the 16-key chunks holding a large probability.
-template <int D>
+// NW waves of 32 rows; NS = 3 stages (96 KB: one 8-wave workgroup per CU)
+// or 2 (64 KB: two 4-wave workgroups per CU).
+template <int D, int NW, int NS>
 void launch_hm(const AttnArgs& a, int n, hipStream_t s) {
-  constexpr int NW = kFwdRowsBf16 / 32;
   const int hm = !(a.hilo & kHiloDq) ? 0 : (a.hilo & kHiloAdaptive) ? 2 : 1;
-  if (hm == 0) hipLaunchKernelGGL((bwd_dq_kernel<D, NW, 0>), dim3(n), dim3(NW * 64), 0, s, a);
-  else if (hm == 1) hipLaunchKernelGGL((bwd_dq_kernel<D, NW, 1>), dim3(n), dim3(NW * 64), 0, s, a);
-  else hipLaunchKernelGGL((bwd_dq_kernel<D, NW, 2>), dim3(n), dim3(NW * 64), 0, s, a);
+  if (hm == 0) hipLaunchKernelGGL((bwd_dq_kernel<D, NW, NS, 0>), dim3(n), dim3(NW * 64), 0, s, a);
+  else if (hm == 1) hipLaunchKernelGGL((bwd_dq_kernel<D, NW, NS, 1>), dim3(n), dim3(NW * 64), 0, s, a);
+  else hipLaunchKernelGGL((bwd_dq_kernel<D, NW, NS, 2>), dim3(n), dim3(NW * 64), 0, s, a);
+}
+
+template <int D>
+void launch_rows(const AttnArgs& a, int rows, int n, hipStream_t s) {
+  if (rows == kQRowsShortBf16) launch_hm<D, kQRowsShortBf16 / 32, 2>(a, n, s);
+  else launch_hm<D, kQRowsLongBf16 / 32, 3>(a, n, s);
 }
 
 }  // namespace
 
-// a.total_tiles / qr[i].tile0 / ntiles must describe kFwdRowsBf16-row query tiles.
-hipError_t launch_bwd_dq_bf16(const AttnArgs& a, int head_dim, hipStream_t s) {
+// a.total_tiles / qr[i].tile0 / ntiles must describe query tiles of `rows` rows.
+hipError_t launch_bwd_dq_bf16(const AttnArgs& a, int head_dim, int rows, hipStream_t s) {
   const int n = a.total_tiles * a.heads * a.batch;
   if (n == 0) return hipSuccess;
-  if (head_dim == 128) launch_hm<128>(a, n, s);
-  else launch_hm<64>(a, n, s);
+  if (head_dim == 128) launch_rows<128>(a, rows, n, s);
+  else launch_rows<64>(a, rows, n, s);
   return hipGetLastError();
 }
 

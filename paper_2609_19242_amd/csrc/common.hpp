@@ -191,13 +191,13 @@ __device__ inline int xcd_remap(int wg, int n) {
 }
 
 // Launchers (defined in the .hip files).  All return hipSuccess or the launch error.
-hipError_t launch_fwd_bf16(const AttnArgs& a, int head_dim, hipStream_t s);
+hipError_t launch_fwd_bf16(const AttnArgs& a, int head_dim, int rows, hipStream_t s);
 hipError_t launch_fwd_f32(const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_merge(const MergeArgs& a, int head_dim, int part_dtype, int out_dtype, hipStream_t s);
 hipError_t launch_bwd_pre(const AttnArgs& a, int head_dim, hipStream_t s);  // fp32 path
 hipError_t launch_bwd_bf16(const AttnArgs& a, int head_dim, hipStream_t s);
 hipError_t launch_bwd_dkdv(const AttnArgs& a, hipStream_t s);
-hipError_t launch_bwd_dq_bf16(const AttnArgs& a, int head_dim, hipStream_t s);
+hipError_t launch_bwd_dq_bf16(const AttnArgs& a, int head_dim, int rows, hipStream_t s);
 hipError_t launch_bwd_f32(const AttnArgs& a, int head_dim, hipStream_t s);
 
 // The walk of a key tile of the scheduled dK/dV kernel over its visible query
@@ -276,7 +276,16 @@ inline bool dkdv_uses_scheduled_kernel(int dtype_bf16, int head_dim, int hilo, i
 }
 
 // Tile heights the launchers use (the C ABI fills ntiles/tile0 with them).
-constexpr int kFwdRowsBf16 = 256;  // query rows per forward / dQ workgroup (8 waves x 32)
+// The bf16 forward and dQ kernels take 256 query rows per workgroup (8 waves,
+// one workgroup per CU) when some row of the call can see many keys, and 128
+// (4 waves, two workgroups per CU) when none can see more than the kernel's
+// short-walk limit: on short walks one workgroup's start-up and barriers
+// overlap the other's products, which outweighs copying every K/V tile for
+// half as many rows; on long walks the extra copies cost more.
+constexpr int kQRowsLongBf16 = 256;
+constexpr int kQRowsShortBf16 = 128;
+constexpr int64_t kFwdShortWalk = 16384;  // keys a row may see for the 128-row forward
+constexpr int64_t kDqShortWalk = 8192;    // ... and for the 128-row dQ kernel
 constexpr int kFwdRowsF32 = 128;
 constexpr int kBwdKeysBf16 = 128;  // key rows per backward workgroup (4 waves x 32)
 constexpr int kBwdKeysF32 = 128;

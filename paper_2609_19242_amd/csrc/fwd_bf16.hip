@@ -5,7 +5,10 @@
 // eq:context-parallel-attention), flash-style with an online softmax, so the
 // partial attention of App. C (one key range) is the same kernel with n_k = 1.
 //
-// Workgroup: NW waves, 32 query rows per wave (BM = 32*NW rows of one head).
+// Workgroup: NW waves, 32 query rows per wave (BM = 32*NW rows of one head):
+// 8 waves and three K/V stages on long walks (one workgroup per CU), 4 waves
+// and two stages on short ones (two workgroups per CU, so that one's start-up
+// and barriers overlap the other's products).
 // Per key tile (BN = 64 keys) each wave computes S^T = K Q^T with
 // v_mfma_f32_32x32x16_bf16 (K from LDS as the A operand, the wave's Q rows held
 // in registers as B), so a lane owns one query row and 32 of the tile's keys;
@@ -13,8 +16,8 @@
 // permlane32 swap and the row sum stays split across the two half-waves until
 // the epilogue.  O^T += V^T P^T uses the probabilities straight from the S^T
 // registers as the B operand, and V^T fragments come from the row-major V tile
-// through LDS transpose reads.  K/V tiles arrive by LDS-DMA copies two tiles
-// ahead into three stages, one barrier per tile, their rows stored unpadded
+// through LDS transpose reads.  K/V tiles arrive by LDS-DMA copies NS - 1
+// tiles ahead into NS stages, one barrier per tile, their rows stored unpadded
 // with a row-dependent XOR permutation of 16-byte chunks under which both the
 // row reads and the transpose reads are free of bank conflicts.  A wave none
 // of whose rows sees a partly visible tile skips it.
@@ -32,8 +35,9 @@ namespace {
 constexpr float kLn2 = 0.69314718055994530942f;
 constexpr float kSumLimit = 18446744073709551616.f;  // 2^64: a lane's tile sum of p above which m_run moves
 
-template <int D, int NW, int HM>
-__global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
+template <int D, int NW, int NS, int HM>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2))) void fwd_bf16_kernel(
+    const AttnArgs a) {
   constexpr int BM = NW * 32, BN = 64, KS = D / 16, DT = D / 32;
   constexpr uint32_t RB = D * 2, TB = BN * RB;  // row and tile bytes in LDS
   constexpr int STAGE = 2 * BN * D;             // K tile + V tile (elements), swizzled rows
@@ -41,7 +45,7 @@ __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
   // waves 0 .. NW/2 - 1 copy K and the others V, IPW instructions each.
   constexpr int TI = BN * D / 8 / 64, IPW = TI / (NW / 2);
   static_assert(TI % (NW / 2) == 0, "whole copy instructions per wave");
-  __shared__ __attribute__((aligned(256))) bf16 lds[3 * STAGE];
+  __shared__ __attribute__((aligned(256))) bf16 lds[NS * STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, half = lane >> 5;
@@ -88,7 +92,7 @@ __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
     c.have = find_key_tile(a, c.j + 1, qr.stream, pq0, pq1, BN, c.j, c.t, c.t1, c.f0, c.f1);
     return c;
   };
-  // The copy cursor runs two tiles ahead of the compute cursor and carries
+  // The copy cursor runs NS - 1 tiles ahead of the compute cursor and carries
   // the source pointer of its tile (this wave's tensor, batch and KV head
   // applied) and the rows left in its range, so that advancing inside a range
   // is one pointer increment; both are recomputed only when the range changes.
@@ -137,22 +141,25 @@ __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
   const uint32_t yrow = swz_row_part<D>(l32, half);
   const uint32_t ytr0 = swz_tr_part<D>(G, sl, 0), ytr1 = swz_tr_part<D>(G, sl, 8);
 
-  // Three LDS stages, copies two tiles ahead.  At the barrier closing a tile,
-  // every wave has waited for its copies of the next tile (only those of the
-  // tile after it stay in flight) and has finished reading the stage the
-  // following copies overwrite.
+  // NS LDS stages, copies NS - 1 tiles ahead.  At the barrier closing a
+  // tile, every wave has waited for its copies of the next tile (only those
+  // of the NS - 2 tiles after it stay in flight) and has finished reading
+  // the stage the following copies overwrite.  (The compiler makes each
+  // tile's first transpose read wait for every copy in flight, so a third
+  // stage gains nothing over two except a shorter wait at the barrier.)
   KCur c0;
   c0.have = find_key_tile(a, 0, qr.stream, pq0, pq1, BN, c0.j, c0.t, c0.t1, c0.f0, c0.f1);
   CopyCur cp = copy_seek(CopyCur{c0, any_src, 0});
-  copy_tile(lds, cp);
-  cp = copy_next(cp);
-  copy_tile(lds + STAGE, cp);
-  cp = copy_next(cp);
-  vm_wait_barrier<IPW>();
+#pragma unroll
+  for (int s = 0; s < NS - 1; ++s) {
+    copy_tile(lds + s * STAGE, cp);
+    cp = copy_next(cp);
+  }
+  vm_wait_barrier<IPW * (NS - 2)>();
   int cur = 0;
   int lane_lo = 0, lane_w = 0, lane_j = -1;
   while (c0.have) {
-    copy_tile(lds + (cur == 0 ? 2 : cur - 1) * STAGE, cp);
+    copy_tile(lds + (cur == 0 ? NS - 1 : cur - 1) * STAGE, cp);
     const int j = c0.j, t = c0.t, f0 = c0.f0, f1 = c0.f1;
     if (lane_j != j) {  // this lane's visible key interval inside range j
       lane_key_interval(a, j, qr.stream, pq, lane_lo, lane_w);
@@ -322,8 +329,8 @@ __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
       }
     }
 
-    vm_wait_barrier<IPW>();
-    cur = cur == 2 ? 0 : cur + 1;
+    vm_wait_barrier<IPW * (NS - 2)>();
+    cur = cur == NS - 1 ? 0 : cur + 1;
     c0 = next_tile(c0);
     cp = copy_next(cp);
   }
@@ -368,22 +375,29 @@ __global__ __launch_bounds__(NW * 64) void fwd_bf16_kernel(const AttnArgs a) {
 
 // HM of the kernel: 0 single-term P (dS), 1 two-term on every tile, 2
 // two-term on the 16-key chunks holding a large probability.
-template <int D>
+// NW waves of 32 rows; NS = 3 stages (96 KB: one 8-wave workgroup per CU)
+// or 2 (64 KB: two 4-wave workgroups per CU).
+template <int D, int NW, int NS>
 void launch_hm(const AttnArgs& a, int n, hipStream_t s) {
-  constexpr int NW = kFwdRowsBf16 / 32;
   const int hm = !(a.hilo & kHiloPv) ? 0 : (a.hilo & kHiloAdaptive) ? 2 : 1;
-  if (hm == 0) hipLaunchKernelGGL((fwd_bf16_kernel<D, NW, 0>), dim3(n), dim3(NW * 64), 0, s, a);
-  else if (hm == 1) hipLaunchKernelGGL((fwd_bf16_kernel<D, NW, 1>), dim3(n), dim3(NW * 64), 0, s, a);
-  else hipLaunchKernelGGL((fwd_bf16_kernel<D, NW, 2>), dim3(n), dim3(NW * 64), 0, s, a);
+  if (hm == 0) hipLaunchKernelGGL((fwd_bf16_kernel<D, NW, NS, 0>), dim3(n), dim3(NW * 64), 0, s, a);
+  else if (hm == 1) hipLaunchKernelGGL((fwd_bf16_kernel<D, NW, NS, 1>), dim3(n), dim3(NW * 64), 0, s, a);
+  else hipLaunchKernelGGL((fwd_bf16_kernel<D, NW, NS, 2>), dim3(n), dim3(NW * 64), 0, s, a);
+}
+
+template <int D>
+void launch_rows(const AttnArgs& a, int rows, int n, hipStream_t s) {
+  if (rows == kQRowsShortBf16) launch_hm<D, kQRowsShortBf16 / 32, 2>(a, n, s);
+  else launch_hm<D, kQRowsLongBf16 / 32, 3>(a, n, s);
 }
 
 }  // namespace
 
-hipError_t launch_fwd_bf16(const AttnArgs& a, int head_dim, hipStream_t s) {
+hipError_t launch_fwd_bf16(const AttnArgs& a, int head_dim, int rows, hipStream_t s) {
   const int n = a.total_tiles * a.heads * a.batch;
   if (n == 0) return hipSuccess;
-  if (head_dim == 128) launch_hm<128>(a, n, s);
-  else launch_hm<64>(a, n, s);
+  if (head_dim == 128) launch_rows<128>(a, rows, n, s);
+  else launch_rows<64>(a, rows, n, s);
   return hipGetLastError();
 }
 

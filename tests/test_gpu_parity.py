@@ -1,7 +1,7 @@
 """GPU parity: the HIP library (through its C ABI) against the fp64 oracle.
 
 Small shapes span several tiles and ragged tails in every dimension the
-kernels tile (256-row forward query tiles, 64-key forward key tiles, 128-key
+kernels tile (128- and 256-row forward and dQ query tiles, 64-key forward key tiles, 128-key
 backward key tiles, 32-row backward query steps); they cover both readings of
 the clean-to-clean rule, GQA groups, head_dim 64 and 128, batch > 1, the
 degenerate block sizes (1 and L) and rows that see no key.
