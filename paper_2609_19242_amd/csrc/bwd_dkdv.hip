@@ -166,8 +166,8 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
   // ---- work item: (batch, KV head, key range, key tile); heaviest tiles first per XCD
   const int T = a.total_tiles;
   const int logical = xcd_remap(blockIdx.x, T * a.kv_heads * a.batch);
-  const int bk = logical / T;
-  int order = logical - bk * T;
+  int bk, order;
+  pair_and_rank(logical, T, a.kv_heads * a.batch, bk, order);
   const int b = bk / a.kv_heads, kvh = bk - (bk / a.kv_heads) * a.kv_heads;
   int r = a.order[0], t = order;
   for (int n = 0; n < a.n_k; ++n) {

@@ -190,6 +190,27 @@ __device__ inline int xcd_remap(int wg, int n) {
   return (xcd < r) ? xcd * (q + 1) + slot : r * (q + 1) + (xcd - r) * q + slot;
 }
 
+// Logical work id (after xcd_remap) -> (pair, rank) for the key-major dK/dV
+// kernels: T key tiles per (batch, KV head) pair, nbk pairs, the tiles of a
+// pair numbered heaviest first.  When the pairs divide evenly over the 8 XCDs,
+// the m pairs of one XCD are interleaved tile by tile, so that the heaviest
+// tiles of all of them start first on the XCD's CUs (one pair after the other
+// left the second pair's heaviest tiles to start late and end last: 7-8% of
+// the kernel at batch 2 and 4, 4K keys).  Otherwise pairs follow one another.
+// (The query-major kernels keep pairs in sequence: there interleaving puts the
+// K/V of several heads in one XCD's L2 at once and was slower.)
+__device__ inline void pair_and_rank(int logical, int T, int nbk, int& bk, int& rank) {
+  if (nbk > 8 && nbk % 8 == 0) {
+    const int m = nbk >> 3, span = m * T;
+    const int x = logical / span, local = logical - x * span;
+    rank = local / m;
+    bk = x * m + (local - rank * m);
+  } else {
+    bk = logical / T;
+    rank = logical - bk * T;
+  }
+}
+
 // Launchers (defined in the .hip files).  All return hipSuccess or the launch error.
 hipError_t launch_fwd_bf16(const AttnArgs& a, int head_dim, int rows, hipStream_t s);
 hipError_t launch_fwd_f32(const AttnArgs& a, int head_dim, hipStream_t s);

@@ -67,6 +67,10 @@ SMALL = [
     (256, 256, 2, 1, 128, 1),
     (200, 8, 8, 2, 128, 1),
     (520, 40, 2, 1, 128, 1),
+    # batch x KV heads a multiple of 8 above 8: the dK/dV kernels interleave the
+    # (batch, KV head) pairs that share an XCD (2 per XCD here, 3 below)
+    (200, 8, 16, 8, 128, 2),
+    (150, 10, 8, 8, 64, 3),
 ]
 
 
