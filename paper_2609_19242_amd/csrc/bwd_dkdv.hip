@@ -202,8 +202,6 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
       kf[s] = __builtin_bit_cast(bf16x8, buf_load16(rk, off + 32 * s));
       vf[s] = __builtin_bit_cast(bf16x8, buf_load16(rv, off + 32 * s));
     }
-#pragma unroll
-    for (int s = 0; s < kKS; ++s) asm volatile("" : "+a"(kf[s]), "+a"(vf[s]));
   }
   // dK^T / dV^T accumulators (AGPRs, written only by the inline-assembly MFMAs)
   f32x16 dka[kDT], dva[kDT];
@@ -609,6 +607,11 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
   copy_step(1, 1);
   copy_step(2, 2);
   asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(kIPW + 1) : "memory");  // steps 0 and 1 landed
+  // K and V are pinned in AGPRs only now: pinning reads them, so their loads
+  // (issued first) are waited for here, after the walk set-up and the first
+  // copies, instead of before them.
+#pragma unroll
+  for (int s = 0; s < kKS; ++s) asm volatile("" : "+a"(kf[s]), "+a"(vf[s]));
   load_starts(0, 0);
 #pragma unroll
   for (int i = 0; i < RA; ++i) {
@@ -641,9 +644,9 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
   // ---- epilogue: dK = scale dK^T^T, dV (bf16 or fp32); unseen keys get zeros
 #pragma unroll
   for (int d = 0; d < kDT; ++d) asm volatile("" : "+a"(dka[d]), "+a"(dva[d]));
-  if (key_ok) {
-    const int64_t off = (((int64_t)b * kr.bstride + key0 + mykey) * HKV + kvh) * kD;
-    if (a.out_f32) {
+  if (a.out_f32) {
+    if (key_ok) {
+      const int64_t off = (((int64_t)b * kr.bstride + key0 + mykey) * HKV + kvh) * kD;
       float* dkp = (float*)kr.dk + off;
       float* dvp = (float*)kr.dv + off;
 #pragma unroll
@@ -659,22 +662,38 @@ __global__ __launch_bounds__(256) void dkdv_kernel(const AttnArgs a) {
           *(f32x4*)(dkp + 32 * d + 8 * g4 + 4 * half) = vk;
           *(f32x4*)(dvp + 32 * d + 8 * g4 + 4 * half) = vv;
         }
-    } else {
-      bf16* dkp = (bf16*)kr.dk + off;
-      bf16* dvp = (bf16*)kr.dv + off;
+    }
+  } else {
+    // Each wave's 32 rows of dK and dV go through its own 16 KB of LDS (in the
+    // Q stages, free once every wave has left the walk), so that a store
+    // writes 4 whole rows instead of 16 bytes of each of 32 rows.  Chunk c
+    // (16 bytes) of row r sits at chunk c ^ (r & 15): conflict-free reads.
+    asm volatile("s_barrier" ::: "memory");
+    const uint32_t sw = L0 + kQRegion + (uint32_t)w * 16384u;
 #pragma unroll
-      for (int d = 0; d < kDT; ++d)
+    for (int d = 0; d < kDT; ++d)
 #pragma unroll
-        for (int g4 = 0; g4 < 4; ++g4) {
-          bf16x4 vk, vv;
+      for (int g4 = 0; g4 < 4; ++g4) {
+        bf16x4 vk, vv;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            vk[e] = to_bf16(dka[d][4 * g4 + e] * a.scale);
-            vv[e] = to_bf16(dva[d][4 * g4 + e]);
-          }
-          *(bf16x4*)(dkp + 32 * d + 8 * g4 + 4 * half) = vk;
-          *(bf16x4*)(dvp + 32 * d + 8 * g4 + 4 * half) = vv;
+        for (int e = 0; e < 4; ++e) {
+          vk[e] = to_bf16(dka[d][4 * g4 + e] * a.scale);
+          vv[e] = to_bf16(dva[d][4 * g4 + e]);
         }
+        const uint32_t o = (uint32_t)l32 * 256u + (((uint32_t)(4 * d + g4) ^ (uint32_t)(l32 & 15)) * 16u) + 8u * half;
+        lds_store8(sw + o, vk);
+        lds_store8(sw + 8192u + o, vv);
+      }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int r = i * 4 + (lane >> 4), c = lane & 15;
+      const uint32_t o = (uint32_t)r * 256u + (((uint32_t)c ^ (uint32_t)(r & 15)) * 16u);
+      const bf16x8 xk = lds_load16(sw + o), xv = lds_load16(sw + 8192u + o);
+      if (w * 32 + r < nk) {
+        const int64_t go = (((int64_t)b * kr.bstride + key0 + w * 32 + r) * HKV + kvh) * kD + c * 8;
+        *(bf16x8*)((bf16*)kr.dk + go) = xk;
+        *(bf16x8*)((bf16*)kr.dv + go) = xv;
+      }
     }
   }
 }

@@ -99,6 +99,9 @@ __device__ __forceinline__ uint32_t swz_src_offset(int slot, int64_t row_stride)
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)p;
 }
+__device__ __forceinline__ void lds_store8(uint32_t a, bf16x4 v) {
+  *(__attribute__((address_space(3))) bf16x4*)(uintptr_t)a = v;
+}
 __device__ __forceinline__ bf16x8 lds_load16(uint32_t a) {
   return *(__attribute__((address_space(3))) const bf16x8*)(uintptr_t)a;
 }
