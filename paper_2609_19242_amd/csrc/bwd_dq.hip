@@ -337,10 +337,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
   // the workgroup's LDS is released.
   __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
 
-  if (row_ok) {
-    const int64_t orow = (((int64_t)it.b * qr.bstride + my_row) * H + it.h) * D;
-    if (a.out_f32) {
-      float* op = (float*)qr.dq + orow;
+  if (a.out_f32) {
+    if (row_ok) {
+      float* op = (float*)qr.dq + (((int64_t)it.b * qr.bstride + my_row) * H + it.h) * D;
 #pragma unroll
       for (int d = 0; d < DT; ++d)
 #pragma unroll
@@ -350,18 +349,27 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
           for (int e = 0; e < 4; ++e) v[e] = acc[d][g4 * 4 + e] * a.scale;
           *(f32x4*)(op + 32 * d + 8 * g4 + 4 * half) = v;
         }
-    } else {
-      bf16* op = (bf16*)qr.dq + orow;
-#pragma unroll
-      for (int d = 0; d < DT; ++d)
-#pragma unroll
-        for (int g4 = 0; g4 < 4; ++g4) {
-          bf16x4 v;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = to_bf16(acc[d][g4 * 4 + e] * a.scale);
-          *(bf16x4*)(op + 32 * d + 8 * g4 + 4 * half) = v;
-        }
     }
+  } else if constexpr (HM != 2) {
+    // bf16 dQ through LDS, as the forward's O.
+    asm volatile("s_barrier" ::: "memory");
+    const int wrow0 = row0 + w * 32;
+    store_rows_bf16_via_lds<D>(
+        lds_addr(lds) + (uint32_t)w * (D * 64), [&](int d, int g4, int e) { return acc[d][g4 * 4 + e] * a.scale; },
+        (bf16*)qr.dq + (((int64_t)it.b * qr.bstride + wrow0) * H + it.h) * D, H * D, qr.len - wrow0, lane);
+  } else if (row_ok) {
+    // The adaptive two-term kernel stores directly: the staged form needs the
+    // last few registers it has and made it spill.
+    bf16* op = (bf16*)qr.dq + (((int64_t)it.b * qr.bstride + my_row) * H + it.h) * D;
+#pragma unroll
+    for (int d = 0; d < DT; ++d)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        bf16x4 v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = to_bf16(acc[d][g4 * 4 + e] * a.scale);
+        *(bf16x4*)(op + 32 * d + 8 * g4 + 4 * half) = v;
+      }
   }
 }
 

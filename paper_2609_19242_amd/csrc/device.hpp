@@ -150,4 +150,36 @@ namespace bdlm {
 __device__ __forceinline__ void buf_atomic_add(__amdgpu_buffer_rsrc_t r, uint32_t byte_off, float v) {
   __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(v, r, byte_off, 0, 0);
 }
+
+// A wave's 32 rows x D columns held the MFMA-accumulator way (the lanes l32
+// and l32 + 32 own row l32; element e of fragment (dt, g4) is column
+// 32 dt + 8 g4 + 4 half + e), written to global memory as bf16 through the
+// wave's D * 64 bytes of LDS at sw: the lanes store their 8-byte pieces, then
+// every global store writes 64 / (D / 8) whole rows instead of 16 bytes of
+// each of 32 rows.  16-byte chunk c of row r sits at chunk c ^ (r % (D / 8)),
+// so the row reads are conflict-free.  Row r goes to rows + r * row_stride
+// (elements) when r < nrows.  Nobody else may use those LDS bytes meanwhile.
+template <int D, class V>
+__device__ __forceinline__ void store_rows_bf16_via_lds(uint32_t sw, V&& value, bf16* rows, int64_t row_stride,
+                                                        int nrows, int lane) {
+  constexpr int CH = D / 8, RPI = 64 / CH;
+  const int l32 = lane & 31, half = lane >> 5;
+#pragma unroll
+  for (int dt = 0; dt < D / 32; ++dt)
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4) {
+      bf16x4 v;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = to_bf16(value(dt, g4, e));
+      const uint32_t c = (uint32_t)((4 * dt + g4) ^ (l32 & (CH - 1)));
+      lds_store8(sw + (uint32_t)l32 * (D * 2) + c * 16u + 8u * half, v);
+    }
+#pragma unroll
+  for (int i = 0; i < 32 / RPI; ++i) {
+    const int r = i * RPI + lane / CH, c = lane % CH;
+    const bf16x8 x = lds_load16(sw + (uint32_t)r * (D * 2) + (uint32_t)(c ^ (r & (CH - 1))) * 16u);
+    if (r < nrows) *(bf16x8*)(rows + r * row_stride + c * 8) = x;
+  }
+}
+
 }  // namespace bdlm

@@ -342,10 +342,9 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
   const float l_tot = l_run + partner(l_run);
   const bool empty = !(l_tot > 0.f);
   const float inv = empty ? 0.f : 1.f / l_tot;
-  if (my_row < qr.len) {
-    const int64_t orow = (((int64_t)it.b * qr.bstride + my_row) * H + it.h) * D;
-    if (a.out_f32) {
-      float* op = (float*)qr.o + orow;
+  if (a.out_f32) {
+    if (my_row < qr.len) {
+      float* op = (float*)qr.o + (((int64_t)it.b * qr.bstride + my_row) * H + it.h) * D;
 #pragma unroll
       for (int d = 0; d < DT; ++d)
 #pragma unroll
@@ -355,18 +354,17 @@ __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
           for (int e = 0; e < 4; ++e) v[e] = acc[d][g4 * 4 + e] * inv;
           *(f32x4*)(op + 32 * d + 8 * g4 + 4 * half) = v;
         }
-    } else {
-      bf16* op = (bf16*)qr.o + orow;
-#pragma unroll
-      for (int d = 0; d < DT; ++d)
-#pragma unroll
-        for (int g4 = 0; g4 < 4; ++g4) {
-          bf16x4 v;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = to_bf16(acc[d][g4 * 4 + e] * inv);
-          *(bf16x4*)(op + 32 * d + 8 * g4 + 4 * half) = v;
-        }
     }
+  } else {
+    // bf16 O through LDS (the stages are free: every wave's copies have landed
+    // and every wave has left the walk once all meet this barrier).
+    asm volatile("s_barrier" ::: "memory");
+    const int wrow0 = row0 + w * 32;
+    store_rows_bf16_via_lds<D>(
+        lds_addr(lds) + (uint32_t)w * (D * 64), [&](int d, int g4, int e) { return acc[d][g4 * 4 + e] * inv; },
+        (bf16*)qr.o + (((int64_t)it.b * qr.bstride + wrow0) * H + it.h) * D, H * D, qr.len - wrow0, lane);
+  }
+  if (my_row < qr.len) {
     if (half == 0)
       qr.lse[((int64_t)it.b * H + it.h) * qr.bstride + my_row] =
           empty ? -INFINITY : (m_run + log2f(l_tot)) * kLn2;
