@@ -194,6 +194,23 @@ bdlm_status bdlm_lse_merge(int64_t batch, int64_t rows, int32_t heads, int32_t h
                            const float* const* lse_parts, int32_t part_dtype,
                            void* o, float* lse, int32_t out_dtype, hipStream_t stream);
 
+/*
+ * bdlm_lse_merge over rows laid out with batch strides, as the attention calls
+ * write them (bdlm_range.batch_stride): part element (b, i, h, :) of O_j is at
+ * row b * part_batch_stride + i of o_parts[j], z_j(b, h, i) at
+ * (b * heads + h) * part_batch_stride + i of lse_parts[j]; the outputs likewise
+ * with out_batch_stride.  A stride of 0 means rows (dense, as bdlm_lse_merge).
+ * Strides below rows give BDLM_ERR_INVALID, above 2^30 BDLM_ERR_UNSUPPORTED;
+ * otherwise the contract of bdlm_lse_merge, which is this call with both
+ * strides 0.  Padding rows between batch elements are neither read nor written.
+ */
+bdlm_status bdlm_lse_merge_strided(int64_t batch, int64_t rows, int32_t heads, int32_t head_dim,
+                                   int32_t n_parts, const void* const* o_parts,
+                                   const float* const* lse_parts, int32_t part_dtype,
+                                   int64_t part_batch_stride, void* o, float* lse,
+                                   int32_t out_dtype, int64_t out_batch_stride,
+                                   hipStream_t stream);
+
 /* Workspace bytes bdlm_attn_bwd needs for these query ranges: per range two
  * fp32 arrays of batch * len * heads values (each rounded up to 256 bytes),
  * LSE * log2(e) and the row dots D = rowsum(dO * O).  Ranges whose

@@ -93,6 +93,9 @@ def lib() -> ctypes.CDLL:
         L.bdlm_attn_partial_fwd.argtypes = [ctypes.POINTER(Problem), Range, _VP, _VP, _VP, Range, _VP, _VP, _VP]
         L.bdlm_lse_merge.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
                                      _PP, _PP, ctypes.c_int32, _VP, _VP, ctypes.c_int32, _VP]
+        L.bdlm_lse_merge_strided.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                             ctypes.c_int32, _PP, _PP, ctypes.c_int32, ctypes.c_int64, _VP, _VP,
+                                             ctypes.c_int32, ctypes.c_int64, _VP]
         L.bdlm_attn_bwd_workspace_bytes.argtypes = [ctypes.POINTER(Problem), ctypes.c_int32, ctypes.POINTER(Range)]
         L.bdlm_attn_bwd_workspace_bytes.restype = ctypes.c_size_t
         L.bdlm_attn_bwd.argtypes = [ctypes.POINTER(Problem), ctypes.c_int32, ctypes.POINTER(Range), _PP, _PP, _PP,
@@ -110,8 +113,8 @@ def lib() -> ctypes.CDLL:
         L.bdlm_timing_collect.restype = ctypes.c_int32
         L.bdlm_kernel_name.argtypes = [ctypes.c_int32]
         L.bdlm_kernel_name.restype = ctypes.c_char_p
-        for name in ("bdlm_attn_fwd", "bdlm_attn_partial_fwd", "bdlm_lse_merge", "bdlm_attn_bwd",
-                     "bdlm_attn_bwd_noalloc"):
+        for name in ("bdlm_attn_fwd", "bdlm_attn_partial_fwd", "bdlm_lse_merge", "bdlm_lse_merge_strided",
+                     "bdlm_attn_bwd", "bdlm_attn_bwd_noalloc"):
             getattr(L, name).restype = ctypes.c_int
         _LIB = L
     return _LIB
@@ -197,8 +200,35 @@ def attn_partial_fwd(p: Problem, qr: Range, q, o, lse, kr: Range, k, v, stream=N
                                        _stream(stream)))
 
 
+def _batch_stride(name, t, dtype, shape, lse_layout):
+    """Rows between batch elements of ``t``: a ``[batch][rows][heads][d]`` (or, with ``lse_layout``,
+    ``[batch][heads][rows]``) tensor or view whose rows are packed as in a tensor of ``stride`` rows
+    per batch element, e.g. one range's half of a joint output."""
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor, got {type(t).__name__}")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    st = t.stride()
+    if lse_layout:
+        B, H, R = shape
+        S = st[1] if H > 1 else (st[0] if B > 1 else R)
+        ok = (R <= 1 or st[2] == 1) and (B <= 1 or st[0] == H * S)
+    else:
+        B, R, H, D = shape
+        S = st[0] // (H * D) if B > 1 else R
+        ok = st[3] == 1 and (H <= 1 or st[2] == D) and (R <= 1 or st[1] == H * D) and (B <= 1 or st[0] == S * H * D)
+    if not ok or S < R:
+        raise ValueError(f"{name} must hold its rows packed (only the batch stride may exceed the row count)")
+    return S
+
+
 def lse_merge(o_parts, lse_parts, o, lse, stream=None):
-    """``bdlm_lse_merge`` of partials shaped ``[batch][rows][heads][d]`` / ``[batch][heads][rows]``."""
+    """``bdlm_lse_merge_strided`` of partials shaped ``[batch][rows][heads][d]`` / ``[batch][heads][rows]``.
+
+    Each tensor may be a view whose batch elements lie further apart than ``rows`` (one range of a
+    joint output, say); the parts share one batch stride, ``o`` and ``lse`` another."""
     if not isinstance(o, torch.Tensor) or o.dim() != 4:
         raise ValueError("o must be a [batch][rows][heads][head_dim] tensor")
     B, R, H, D = o.shape
@@ -207,15 +237,21 @@ def lse_merge(o_parts, lse_parts, o, lse, stream=None):
     _dtype_code(o.dtype)
     pdt = o_parts[0].dtype
     _dtype_code(pdt)
+    strides = set()
     for j, (op, lp) in enumerate(zip(o_parts, lse_parts)):
-        _expect(f"o_parts[{j}]", op, pdt, o.shape)
-        _expect(f"lse_parts[{j}]", lp, torch.float32, (B, H, R))
-    _expect("o", o, o.dtype, o.shape)
-    _expect("lse", lse, torch.float32, (B, H, R))
+        strides.add(_batch_stride(f"o_parts[{j}]", op, pdt, o.shape, False))
+        strides.add(_batch_stride(f"lse_parts[{j}]", lp, torch.float32, (B, H, R), True))
+    if len(strides) != 1:
+        raise ValueError("the partials and their LSEs must share one batch stride")
+    so = _batch_stride("o", o, o.dtype, o.shape, False)
+    if _batch_stride("lse", lse, torch.float32, (B, H, R), True) != so:
+        raise ValueError("o and lse must share one batch stride")
     _on_device(o.device, o=o, lse=lse, **{f"o_parts[{j}]": t for j, t in enumerate(o_parts)},
                **{f"lse_parts[{j}]": t for j, t in enumerate(lse_parts)})
-    _check(lib().bdlm_lse_merge(B, R, H, D, len(o_parts), _parr(o_parts), _parr(lse_parts), _dtype_code(pdt),
-                                _ptr(o), _ptr(lse), _dtype_code(o.dtype), _stream(stream)))
+    # views: their addresses are taken as they are (the layout was checked above)
+    _check(lib().bdlm_lse_merge_strided(B, R, H, D, len(o_parts), _parr([t.data_ptr() for t in o_parts]),
+                                        _parr([t.data_ptr() for t in lse_parts]), _dtype_code(pdt), strides.pop(),
+                                        o.data_ptr(), lse.data_ptr(), _dtype_code(o.dtype), so, _stream(stream)))
 
 
 def attn_bwd_workspace_bytes(p: Problem, q_ranges: Sequence[Range]) -> int:

@@ -275,9 +275,24 @@ bdlm_status bdlm_attn_partial_fwd(const bdlm_problem* p, bdlm_range qr, const vo
 bdlm_status bdlm_lse_merge(int64_t batch, int64_t rows, int32_t heads, int32_t head_dim, int32_t n_parts,
                            const void* const* o_parts, const float* const* lse_parts, int32_t part_dtype, void* o,
                            float* lse, int32_t out_dtype, hipStream_t stream) {
+  return bdlm_lse_merge_strided(batch, rows, heads, head_dim, n_parts, o_parts, lse_parts, part_dtype, 0, o, lse,
+                                out_dtype, 0, stream);
+}
+
+bdlm_status bdlm_lse_merge_strided(int64_t batch, int64_t rows, int32_t heads, int32_t head_dim, int32_t n_parts,
+                                   const void* const* o_parts, const float* const* lse_parts, int32_t part_dtype,
+                                   int64_t part_batch_stride, void* o, float* lse, int32_t out_dtype,
+                                   int64_t out_batch_stride, hipStream_t stream) {
   if (batch < 1 || rows < 0 || heads < 1)
     return fail(BDLM_ERR_INVALID, "bad merge shape batch=%lld rows=%lld heads=%d", (long long)batch,
                 (long long)rows, heads);
+  const int64_t ps = part_batch_stride == 0 ? rows : part_batch_stride;
+  const int64_t os = out_batch_stride == 0 ? rows : out_batch_stride;
+  if (ps < rows || os < rows)
+    return fail(BDLM_ERR_INVALID, "merge batch strides %lld / %lld below rows=%lld", (long long)part_batch_stride,
+                (long long)out_batch_stride, (long long)rows);
+  if (ps > kMaxPos || os > kMaxPos)
+    return fail(BDLM_ERR_UNSUPPORTED, "merge batch stride above 2^30");
   if (head_dim != 64 && head_dim != 128)
     return fail(BDLM_ERR_UNSUPPORTED, "head_dim %d not supported (64 or 128)", head_dim);
   constexpr int64_t kMaxUnits = ((int64_t)1 << 31) - 1;  // (row, head) pairs: the grid stays below 2^31 workgroups
@@ -294,6 +309,8 @@ bdlm_status bdlm_lse_merge(int64_t batch, int64_t rows, int32_t heads, int32_t h
   a.heads = heads;
   a.rows = rows;
   a.batch = batch;
+  a.pstride = ps;
+  a.ostride = os;
   if (rows > 0) {
     bdlm_status st;
     if ((st = check_ptr(o, "o", 0)) != BDLM_OK) return st;

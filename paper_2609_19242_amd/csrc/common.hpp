@@ -171,6 +171,7 @@ struct MergeArgs {
   int32_t heads;
   int64_t rows;
   int64_t batch;
+  int64_t pstride, ostride;  // rows between batch elements in the parts and in the output (>= rows)
   const void* o_parts[kMaxParts];
   const float* lse_parts[kMaxParts];
   void* o;

@@ -82,8 +82,10 @@ __global__ __launch_bounds__(256) void merge_kernel(const MergeArgs a, uint32_t 
   const int h = (int)(rh % a.heads);
   const int64_t brow = rh / a.heads;
   const int64_t row = brow % a.rows, b = brow / a.rows;
-  const int64_t lse_idx = (b * a.heads + h) * a.rows + row;
-  const int64_t o_off = rh * D + chunk * 8;
+  const int64_t lse_idx = (b * a.heads + h) * a.pstride + row;            // parts' z
+  const int64_t o_off = ((b * a.pstride + row) * a.heads + h) * D + chunk * 8;  // parts' O
+  const int64_t lse_out = (b * a.heads + h) * a.ostride + row;
+  const int64_t out_off = ((b * a.ostride + row) * a.heads + h) * D + chunk * 8;
   const int n = a.n_parts;
 
   // The parts' z for this (row, head).
@@ -164,8 +166,8 @@ __global__ __launch_bounds__(256) void merge_kernel(const MergeArgs a, uint32_t 
   const float inv = empty ? 0.f : 1.f / den;
 #pragma unroll
   for (int e = 0; e < 8; ++e) num[e] *= inv;
-  store8<TO>((TO*)a.o + o_off, num);
-  if (chunk == 0) a.lse[lse_idx] = empty ? -INFINITY : m + logf(den);
+  store8<TO>((TO*)a.o + out_off, num);
+  if (chunk == 0) a.lse[lse_out] = empty ? -INFINITY : m + logf(den);
 }
 
 template <int D, bool BUF>
@@ -181,7 +183,7 @@ hipError_t launch_db(const MergeArgs& a, int pt, int ot, uint32_t part_bytes, hi
 
 template <int D>
 hipError_t launch_d(const MergeArgs& a, int pt, int ot, hipStream_t s) {
-  const uint64_t bytes = (uint64_t)a.batch * a.rows * a.heads * D * (pt == 0 ? 2 : 4);
+  const uint64_t bytes = (uint64_t)((a.batch - 1) * a.pstride + a.rows) * a.heads * D * (pt == 0 ? 2 : 4);
   if (bytes <= 0xffff0000ull) return launch_db<D, true>(a, pt, ot, (uint32_t)bytes, s);
   return launch_db<D, false>(a, pt, ot, 0u, s);
 }

@@ -99,6 +99,11 @@ def test_merge_and_bwd_validation():
     assert L.bdlm_lse_merge(1, 8, 2, 128, 33, parts, parts, 0, FAKE, FAKE, 0, None) == -2
     assert L.bdlm_lse_merge(1, 8, 2, 80, 1, parts, parts, 0, FAKE, FAKE, 0, None) == -2
     assert L.bdlm_lse_merge(1, 8, 2, 128, 1, parts, parts, 0, FAKE, FAKE + 64, 0, None) == -1  # o aliases a part
+    # strided form: batch strides below the row count are invalid, above 2^30 unsupported
+    assert L.bdlm_lse_merge_strided(2, 8, 2, 128, 1, parts, parts, 0, 7, FAKE + 4096, FAKE + 8192, 0, 0, None) == -1
+    assert L.bdlm_lse_merge_strided(2, 8, 2, 128, 1, parts, parts, 0, 0, FAKE + 4096, FAKE + 8192, 0, 5, None) == -1
+    assert L.bdlm_lse_merge_strided(2, 8, 2, 128, 1, parts, parts, 0, 1 << 31, FAKE + 4096, FAKE + 8192, 0, 0,
+                                    None) == -2
     p = _prob()
     qr = [Range(CORRUPTED, 0, 64)]
     need = bd.attn_bwd_workspace_bytes(p, qr)

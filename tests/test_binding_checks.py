@@ -104,3 +104,25 @@ def test_merge_rejects_mismatched_parts():
         bd.lse_merge(parts, [torch.zeros(B, 8, HQ), lse], o, lse.clone())
     with pytest.raises(ValueError, match="must be on"):
         bd.lse_merge(parts, [lse, lse.clone()], o, lse.clone())
+
+
+def test_merge_takes_row_packed_views_with_a_batch_stride():
+    # one range's half of joint outputs [2][2R][H][D] / [2][H][2R]: accepted up to the device check
+    R = 8
+    jo = torch.zeros(2, 2 * R, HQ, D, dtype=torch.bfloat16)
+    jl = torch.zeros(2, HQ, 2 * R)
+    o, lse = torch.zeros(2, R, HQ, D, dtype=torch.bfloat16), torch.zeros(2, HQ, R)
+    with pytest.raises(ValueError, match="must be on"):
+        bd.lse_merge([jo[:, R:], jo[:, :R]], [jl[:, :, R:], jl[:, :, :R]], o, lse)
+    with pytest.raises(ValueError, match="must be on"):
+        bd.lse_merge([torch.zeros_like(o)], [torch.zeros_like(lse)], jo[:, :R], jl[:, :, :R])
+    # not row-packed: heads and rows swapped, every other row
+    with pytest.raises(ValueError, match="rows packed"):
+        bd.lse_merge([torch.zeros(2, HQ, R, D, dtype=torch.bfloat16).transpose(1, 2)], [jl[:, :, R:]], o, lse)
+    with pytest.raises(ValueError, match="rows packed"):
+        bd.lse_merge([jo[:, ::2]], [jl[:, :, ::2]], o, lse)
+    # parts with different batch strides, o and lse with different ones
+    with pytest.raises(ValueError, match="share one batch stride"):
+        bd.lse_merge([jo[:, R:], torch.zeros_like(o)], [jl[:, :, R:], torch.zeros_like(lse)], o, lse)
+    with pytest.raises(ValueError, match="o and lse must share"):
+        bd.lse_merge([torch.zeros_like(o)], [torch.zeros_like(lse)], jo[:, :R], lse)

@@ -287,6 +287,42 @@ def test_merge_kernel_random_partials():
         assert (o[:, :5] == 0).all() and torch.isneginf(lse[:, :, :5]).all()
 
 
+@pytest.mark.parametrize("pdt,odt", [(torch.bfloat16, torch.bfloat16), (torch.float32, torch.float32)],
+                         ids=["bf16", "fp32"])
+def test_merge_of_strided_views(pdt, odt):
+    """bdlm_lse_merge_strided through lse_merge: partials that are row windows of larger tensors
+    (batch stride 700, rows 100..399) merged into a window of another (batch stride 500, rows
+    50..349), every padding row NaN.  The merged rows equal the dense merge of contiguous copies
+    bit for bit and the oracle's merge; no padding row is read into or written."""
+    g = torch.Generator().manual_seed(11)
+    B, R, H, D, J, SP, SO, P0, Q0 = 2, 300, 4, 128, 4, 700, 500, 100, 50
+    os_ = [torch.randn(B, R, H, D, generator=g) for _ in range(J)]
+    ls = [torch.randn(B, H, R, generator=g) * 4 for _ in range(J)]
+    ls[1][:, :, 7:40] = -float("inf")
+    os_[1][:, 7:40] = 0.0
+    big_o = [torch.full((B, SP, H, D), float("nan"), dtype=pdt, device=DEV) for _ in range(J)]
+    big_l = [torch.full((B, H, SP), float("nan"), device=DEV) for _ in range(J)]
+    for j in range(J):
+        big_o[j][:, P0:P0 + R] = os_[j].to(pdt).to(DEV)
+        big_l[j][:, :, P0:P0 + R] = ls[j].to(DEV)
+    out_o = torch.full((B, SO, H, D), float("nan"), dtype=odt, device=DEV)
+    out_l = torch.full((B, H, SO), float("nan"), device=DEV)
+    bd.lse_merge([t[:, P0:P0 + R] for t in big_o], [t[:, :, P0:P0 + R] for t in big_l],
+                 out_o[:, Q0:Q0 + R], out_l[:, :, Q0:Q0 + R])
+    dense_o = torch.empty(B, R, H, D, dtype=odt, device=DEV)
+    dense_l = torch.empty(B, H, R, device=DEV)
+    bd.lse_merge([t[:, P0:P0 + R].contiguous() for t in big_o], [t[:, :, P0:P0 + R].contiguous() for t in big_l],
+                 dense_o, dense_l)
+    torch.cuda.synchronize()
+    assert torch.equal(out_o[:, Q0:Q0 + R], dense_o) and torch.equal(out_l[:, :, Q0:Q0 + R], dense_l)
+    assert torch.isnan(out_o[:, :Q0]).all() and torch.isnan(out_o[:, Q0 + R:]).all()
+    assert torch.isnan(out_l[:, :, :Q0]).all() and torch.isnan(out_l[:, :, Q0 + R:]).all()
+    Or, Lr = oracle.lse_merge([t.to(pdt) for t in os_], ls)
+    tol = torch.float32 if pdt == torch.float32 else torch.bfloat16
+    assert_close(f"strided merge {pdt} O", dense_o, Or, tol)
+    assert_close(f"strided merge {pdt} LSE", dense_l, Lr, tol)
+
+
 def test_empty_rows_partial():
     """Corrupted queries of block 0 over the clean stream: O = 0 exactly, LSE = -inf."""
     L, M, H, D = 256, 32, 2, 128
