@@ -323,6 +323,40 @@ def test_merge_of_strided_views(pdt, odt):
     assert_close(f"strided merge {pdt} LSE", dense_l, Lr, tol)
 
 
+def test_backward_split_over_key_ranges():
+    """A backward over key ranges A and B equals one call over A and one over B: each range's
+    dK/dV bit for bit, and dQ as the sum of the two calls' dQ (fp32, summation order aside).
+    This is how a caller with more key ranges than one call takes splits its backward."""
+    L, M, Hq, Hkv, D = 384, 16, 4, 2, 128
+    q, k, v, do = (t.to(DEV) for t in joint_inputs(L, Hq, Hkv, D, torch.bfloat16, seed=123))
+    o, lse = bd.joint_fwd(q, k, v, M, out_f32=True)
+    p = bd.make_problem(1, L, M, Hq, Hkv, D, torch.bfloat16, out_f32=True)
+    r = bd.joint_ranges(L)
+    halves = lambda t: bd._joint_ptrs(t, L)  # noqa: E731
+    lp = [lse.data_ptr(), lse.data_ptr() + L * 4]
+    ws = torch.empty(bd.attn_bwd_workspace_bytes(p, r), dtype=torch.uint8, device=DEV)
+
+    def run(key_sel):
+        dq = torch.zeros(q.shape, dtype=torch.float32, device=DEV)
+        dk = torch.full(k.shape, float("nan"), dtype=torch.float32, device=DEV)
+        dv = torch.full(v.shape, float("nan"), dtype=torch.float32, device=DEV)
+        kr = [r[i] for i in key_sel]
+        pick = lambda ptrs: [ptrs[i] for i in key_sel]  # noqa: E731
+        bd.attn_bwd(p, r, halves(q), halves(o), lp, halves(do), halves(dq), kr, pick(halves(k)), pick(halves(v)),
+                    pick(halves(dk)), pick(halves(dv)), ws)
+        torch.cuda.synchronize()
+        return dq, dk, dv
+
+    dq, dk, dv = run([0, 1])
+    dq0, dk0, dv0 = run([0])
+    dq1, dk1, dv1 = run([1])
+    rows0 = slice(0, L) if r[0].stream == CORRUPTED else slice(L, 2 * L)
+    rows1 = slice(L, 2 * L) if rows0.start == 0 else slice(0, L)
+    assert torch.equal(dk0[:, rows0], dk[:, rows0]) and torch.equal(dv0[:, rows0], dv[:, rows0])
+    assert torch.equal(dk1[:, rows1], dk[:, rows1]) and torch.equal(dv1[:, rows1], dv[:, rows1])
+    assert_close("split dQ", dq0 + dq1, dq.double().cpu().numpy(), torch.float32)
+
+
 def test_empty_rows_partial():
     """Corrupted queries of block 0 over the clean stream: O = 0 exactly, LSE = -inf."""
     L, M, H, D = 256, 32, 2, 128
