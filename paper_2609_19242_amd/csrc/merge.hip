@@ -69,7 +69,7 @@ __device__ inline void row_broadcast_z(float (&z)[kMaxParts], float za, float zb
 // part below 4 GiB) the loads go through buffer resources, and a part with
 // w_j = 0 is given an out-of-range offset: no branch, and the hardware fetches
 // nothing for it.
-template <int D, typename TI, typename TO, bool BUF>
+template <int D, typename TI, typename TO, bool BUF, bool DENSE>
 __global__ __launch_bounds__(256) void merge_kernel(const MergeArgs a, uint32_t part_bytes) {
   constexpr int CPR = D / 8;
   constexpr int W = sizeof(TI) == 2 ? 1 : 2;  // 16-byte words per thread and part
@@ -82,10 +82,19 @@ __global__ __launch_bounds__(256) void merge_kernel(const MergeArgs a, uint32_t 
   const int h = (int)(rh % a.heads);
   const int64_t brow = rh / a.heads;
   const int64_t row = brow % a.rows, b = brow / a.rows;
-  const int64_t lse_idx = (b * a.heads + h) * a.pstride + row;            // parts' z
-  const int64_t o_off = ((b * a.pstride + row) * a.heads + h) * D + chunk * 8;  // parts' O
-  const int64_t lse_out = (b * a.heads + h) * a.ostride + row;
-  const int64_t out_off = ((b * a.ostride + row) * a.heads + h) * D + chunk * 8;
+  // Element offsets of the parts' z and O and of the outputs; with DENSE both
+  // batch strides equal rows (the 64-bit stride products would delay the loads
+  // of this memory-bound kernel by a few percent).
+  int64_t lse_idx, o_off, lse_out, out_off;
+  if constexpr (DENSE) {
+    lse_idx = lse_out = (b * a.heads + h) * a.rows + row;
+    o_off = out_off = rh * D + chunk * 8;
+  } else {
+    lse_idx = (b * a.heads + h) * a.pstride + row;
+    o_off = ((b * a.pstride + row) * a.heads + h) * D + chunk * 8;
+    lse_out = (b * a.heads + h) * a.ostride + row;
+    out_off = ((b * a.ostride + row) * a.heads + h) * D + chunk * 8;
+  }
   const int n = a.n_parts;
 
   // The parts' z for this (row, head).
@@ -170,14 +179,24 @@ __global__ __launch_bounds__(256) void merge_kernel(const MergeArgs a, uint32_t 
   if (chunk == 0) a.lse[lse_out] = empty ? -INFINITY : m + logf(den);
 }
 
+template <int D, bool BUF, bool DENSE>
+void launch_dbd(const MergeArgs& a, int pt, int ot, uint32_t part_bytes, dim3 grid, hipStream_t s) {
+  if (pt == 0 && ot == 0)
+    hipLaunchKernelGGL((merge_kernel<D, bf16, bf16, BUF, DENSE>), grid, dim3(256), 0, s, a, part_bytes);
+  if (pt == 0 && ot == 1)
+    hipLaunchKernelGGL((merge_kernel<D, bf16, float, BUF, DENSE>), grid, dim3(256), 0, s, a, part_bytes);
+  if (pt == 1 && ot == 0)
+    hipLaunchKernelGGL((merge_kernel<D, float, bf16, BUF, DENSE>), grid, dim3(256), 0, s, a, part_bytes);
+  if (pt == 1 && ot == 1)
+    hipLaunchKernelGGL((merge_kernel<D, float, float, BUF, DENSE>), grid, dim3(256), 0, s, a, part_bytes);
+}
+
 template <int D, bool BUF>
 hipError_t launch_db(const MergeArgs& a, int pt, int ot, uint32_t part_bytes, hipStream_t s) {
   const int64_t total = a.batch * a.rows * a.heads * (D / 8);
   const dim3 grid((unsigned)((total + 255) / 256));
-  if (pt == 0 && ot == 0) hipLaunchKernelGGL((merge_kernel<D, bf16, bf16, BUF>), grid, dim3(256), 0, s, a, part_bytes);
-  if (pt == 0 && ot == 1) hipLaunchKernelGGL((merge_kernel<D, bf16, float, BUF>), grid, dim3(256), 0, s, a, part_bytes);
-  if (pt == 1 && ot == 0) hipLaunchKernelGGL((merge_kernel<D, float, bf16, BUF>), grid, dim3(256), 0, s, a, part_bytes);
-  if (pt == 1 && ot == 1) hipLaunchKernelGGL((merge_kernel<D, float, float, BUF>), grid, dim3(256), 0, s, a, part_bytes);
+  if (a.pstride == a.rows && a.ostride == a.rows) launch_dbd<D, BUF, true>(a, pt, ot, part_bytes, grid, s);
+  else launch_dbd<D, BUF, false>(a, pt, ot, part_bytes, grid, s);
   return hipGetLastError();
 }
 
