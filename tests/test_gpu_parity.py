@@ -88,6 +88,17 @@ def test_joint_small(shape, reading, mode):
                 hilo=HILO_OF_MODE.get(mode, 0))
 
 
+@pytest.mark.parametrize("hilo", ["all", "adaptive"])
+@pytest.mark.parametrize("shape", [SMALL[0], SMALL[4], SMALL[6]], ids=lambda s: "L{}-M{}-H{}x{}-d{}-b{}".format(*s))
+def test_joint_small_two_terms_bf16_outputs(shape, hilo):
+    """Two-term products with bf16 outputs, both output modes against one oracle result: the forward's
+    bf16 O goes through its LDS-staged epilogue, the adaptive dQ kernel stores bf16 dQ directly."""
+    L, M, Hq, Hkv, D, B = shape
+    q, k, v, do = joint_inputs(L, Hq, Hkv, D, torch.bfloat16, batch=B, seed=L + M + D + 7)
+    check_joint(q, k, v, do, M, 0, torch.bfloat16, tag=f"L{L} M{M} two-term {hilo}", outs=("f32", "bf16"),
+                hilo=HILO_OF_MODE["bf16-hilo" if hilo == "all" else "bf16-hilo-adaptive"])
+
+
 @pytest.mark.parametrize("reading", [0, 1], ids=["causal", "block"])
 @pytest.mark.parametrize("hilo", ["all", "adaptive"])
 @pytest.mark.parametrize("Hq", [8, 6], ids=["group4", "group3"])
